@@ -1,0 +1,82 @@
+"""Pins of the oracle's spherical harmonics and Wigner matrices.
+
+* complex harmonics against scipy.special (an independent library routine);
+* real harmonics against the Cartesian closed forms written out below;
+* addition theorem with numpy's Legendre polynomials; quadrature
+  orthonormality; parity Y(-r) = (-1)^l Y(r);
+* Wigner matrices: orthogonality, the homomorphism D(R1 R2) = D(R1) D(R2), and
+  D^1 = P R P^T for the permutation (x, y, z) -> (y, z, x).
+"""
+
+from math import pi, sqrt
+
+import numpy as np
+import pytest
+
+from oracle import sh, wigner
+
+
+def _dirs(n, seed=3):
+    v = np.random.default_rng(seed).standard_normal((n, 3))
+    return v / np.linalg.norm(v, axis=1, keepdims=True)
+
+
+def test_complex_against_scipy():
+    special = pytest.importorskip("scipy.special")
+    if not hasattr(special, "sph_harm_y"):
+        pytest.skip("scipy without sph_harm_y")
+    v = _dirs(50)
+    theta = np.arccos(np.clip(v[:, 2], -1, 1))
+    phi = np.arctan2(v[:, 1], v[:, 0])
+    for l in range(5):
+        ours = sh.sh_complex(l, v)
+        for m in range(-l, l + 1):
+            ref = special.sph_harm_y(l, m, theta, phi)
+            np.testing.assert_allclose(ours[:, m + l], ref, atol=1e-12)
+
+
+def test_real_cartesian_closed_forms():
+    v = _dirs(64)
+    x, y, z = v[:, 0], v[:, 1], v[:, 2]
+    expect = {
+        0: [np.ones_like(x)],
+        1: [sqrt(3) * y, sqrt(3) * z, sqrt(3) * x],
+        2: [sqrt(15) * x * y, sqrt(15) * y * z, sqrt(5) / 2 * (3 * z ** 2 - 1), sqrt(15) * x * z,
+            sqrt(15) / 2 * (x ** 2 - y ** 2)],
+    }
+    for l, cols in expect.items():
+        np.testing.assert_allclose(sh.sh_real(l, v), np.stack(cols, axis=1), atol=1e-13)
+
+
+def test_addition_theorem_and_parity():
+    a, b = _dirs(40, 1), _dirs(40, 2)
+    cosg = np.sum(a * b, axis=1)
+    for l in range(6):
+        ya, yb = sh.sh_real(l, a), sh.sh_real(l, b)
+        pl = np.polynomial.legendre.legval(cosg, [0] * l + [1])
+        np.testing.assert_allclose(np.sum(ya * yb, axis=1), (2 * l + 1) * pl, atol=1e-12)
+        np.testing.assert_allclose(sh.sh_real(l, -a), (-1) ** l * ya, atol=1e-13)
+
+
+def test_quadrature_orthonormality():
+    nodes, weights = np.polynomial.legendre.leggauss(16)
+    n_phi = 32
+    phi = (np.arange(n_phi) + 0.5) * 2 * pi / n_phi
+    ct, ph = np.meshgrid(nodes, phi, indexing="ij")
+    st = np.sqrt(1 - ct * ct)
+    pts = np.stack([st * np.cos(ph), st * np.sin(ph), ct], axis=-1).reshape(-1, 3)
+    wts = (weights[:, None] * np.full(n_phi, 2 * pi / n_phi)[None, :]).reshape(-1)
+    y = sh.sh_real_all(4, pts)
+    gram = (y * wts[:, None]).T @ y / (4 * pi)
+    np.testing.assert_allclose(gram, np.eye(y.shape[1]), atol=1e-12)
+
+
+def test_wigner_properties():
+    rng = np.random.default_rng(11)
+    r1, r2 = wigner.random_rotation(rng), wigner.random_rotation(rng)
+    for l in range(5):
+        d1, d2, d12 = (wigner.wigner_d_real(l, r) for r in (r1, r2, r1 @ r2))
+        np.testing.assert_allclose(d1 @ d1.T, np.eye(2 * l + 1), atol=1e-11)
+        np.testing.assert_allclose(d12, d1 @ d2, atol=1e-11)
+    perm = np.eye(3)[[1, 2, 0]]  # (x, y, z) -> (y, z, x)
+    np.testing.assert_allclose(wigner.wigner_d_real(1, r1), perm @ r1 @ perm.T, atol=1e-12)
