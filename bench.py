@@ -1,0 +1,247 @@
+"""Benchmark: Allegro tensor product forward + backward edges/s on one MI355X.
+
+One step is one pass of the whole hot path over the resident workload:
+allegro_env_embed + allegro_tp_forward + allegro_tp_backward (the backward
+includes the embedding's VJP), all on one HIP stream, inputs already in HBM.
+
+Workload (default): 20,000 atoms uniform in a periodic cube at 0.1 atoms/A^3
+(the number density of liquid water), cutoff 5 A (about 1.05e6 directed edges,
+CSR by center), U = 64 channels, lmax = 2 with full parity (d1 = 18, d2 = 9,
+30 paths, 274 coupling non-zeros); fp32 features drawn N(0, 1), path weights
+N(0, 1/sqrt(30)).  Synthetic data: no dataset of the paper is used.
+
+Prints ONE JSON line.  The roofline object describes the dominant kernel
+(tp_backward): algorithmic bytes per launch over its mean duration, measured
+with HIP events on the stream the library launches on.  cpu_baseline times
+the fp64 oracle (single thread) on a prefix of whole center segments.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads  # noqa: E402
+
+METRIC = "Allegro TP fwd+bwd edges/sec at lmax=2, 64 ch; % of HBM (or MFMA) roofline"
+HBM_PEAK_GBPS = 8000.0
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "tp_backward_headline_traffic.json")
+
+
+def algorithmic_bytes(cfg, n_atoms: int, n_edges: int):
+    """Bytes each kernel must move at least once (fp32 data, int64 row_ptr).
+
+    env_embed:   read w [E,U] and Y [E,d2]; write env [N,U,d2]
+    tp_forward:  read x [E,U,d1] and env; write out [E,U,d1]
+    tp_backward: read x, g [E,U,d1], env, w, Y; write grad_x [E,U,d1],
+                 grad_env [N,U,d2], grad_w [E,U], grad_Y [E,d2]
+    (row_ptr and the path weights add (N+1)*8 and P*U*4 bytes to each.)
+    """
+    d1, d2, n_paths = workloads.dims(cfg.lmax, cfg.full_parity)
+    u = cfg.U
+    small = (n_atoms + 1) * 8 + n_paths * u * 4
+    env_b = 4 * (n_edges * (u + d2) + n_atoms * u * d2) + (n_atoms + 1) * 8
+    fwd_b = 4 * (2 * n_edges * u * d1 + n_atoms * u * d2) + small
+    bwd_b = 4 * (n_edges * (3 * u * d1 + 2 * u + 2 * d2) + 2 * n_atoms * u * d2) + small
+    return {"env_embed": env_b, "tp_forward": fwd_b, "tp_backward": bwd_b}
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in ("paper_2504_16068_amd/csrc/allegro_tp.hip", "paper_2504_16068_amd/csrc/gen_kernels.cpp",
+                "paper_2504_16068_amd/csrc/cg_builder.cpp"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per tp_backward launch from the committed rocprofv3 counters, if they
+    were taken on the current kernel sources and this workload; else None."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    with open(PROFILE_TRAFFIC) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_digest") != kernel_source_digest() or rec.get("workload") != workload:
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def copy_bandwidth(torch, dev, n_bytes=4 << 30, reps=10):
+    src = torch.empty(n_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    sec = a.elapsed_time(b) / 1e3 / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * n_bytes / sec / 1e9
+
+
+def cpu_baseline(graph, host_inputs, max_edges=8192):
+    """Time the fp64 oracle (one thread) on a prefix of whole center segments."""
+    from threadpoolctl import threadpool_limits
+
+    from oracle import tp as otp
+
+    cfg = graph.config
+    n = workloads.segment_prefix(graph.row_ptr, max_edges)
+    e = int(graph.row_ptr[n])
+    x, w, pw, g = host_inputs(e)
+    rp, y = graph.row_ptr[: n + 1], graph.Y[:e]
+    t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        env = otp.env_embed(rp, w, y)
+        t.forward(rp, x, env, pw)
+        t.backward(rp, x, env, pw, g, w, y)
+        sec = time.perf_counter() - t0
+    return {"value": e / sec, "unit": "edges/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} centers ({e} edges) of the same workload: env_embed + forward + backward, "
+                      f"fp64 NumPy, one thread, {sec:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="headline", choices=sorted(workloads.CONFIGS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the tensor product shards by center ranges with no "
+              "communication inside the path, and multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2504_16068_amd as at
+
+    dev = torch.device("cuda:0")
+    graph = workloads.make_graph(args.workload)
+    cfg = graph.config
+    n_atoms, n_edges = graph.n_atoms, graph.n_edges
+    if cfg.host_features:
+        xh, wh, pwh, gh = workloads.host_features(cfg, n_edges)
+        x, w, g = (torch.from_numpy(a).to(dev) for a in (xh, wh, gh))
+    else:
+        x, w, g = workloads.device_features(cfg, n_edges, dev)
+    pw = torch.from_numpy(workloads.path_weights(cfg)).to(dev)
+    rp = torch.from_numpy(graph.row_ptr).to(dev)
+    y = torch.from_numpy(graph.Y).to(dev)
+    plan = at.allegro_tp_plan_create(cfg.lmax, cfg.U, at.ALLEGRO_FULL_PARITY if cfg.full_parity else 0)
+    env = torch.empty((n_atoms, cfg.U, plan.d2), device=dev)
+    out = torch.empty_like(x)
+    grads = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(y))
+
+    def step():
+        at.allegro_env_embed(plan, rp, w, y, env=env)
+        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
+        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record()
+        at.allegro_env_embed(plan, rp, w, y, env=env)
+        ev[k][1].record()
+        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
+        ev[k][2].record()
+        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
+        ev[k][3].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+
+    names = ("env_embed", "tp_forward", "tp_backward")
+    per_kernel_ms = {nm: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
+                     for i, nm in enumerate(names)}
+    ms_per_step = wall * 1e3 / args.steps
+    value = n_edges / (ms_per_step / 1e3)
+
+    algo = algorithmic_bytes(cfg, n_atoms, n_edges)
+    bwd_s = per_kernel_ms["tp_backward"] / 1e3
+    achieved = algo["tp_backward"] / bwd_s / 1e9
+    copy_gbps = copy_bandwidth(torch, dev)
+    traffic = measured_traffic(args.workload)
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{args.workload}: {n_atoms} atoms at 0.1/A^3 in a periodic cube, cutoff {cfg.cutoff} A, "
+                        f"{n_edges} edges (CSR by center), U={cfg.U}, lmax={cfg.lmax}, "
+                        f"{'full' if cfg.full_parity else 'natural'} parity",
+            "atoms": n_atoms, "edges": n_edges, "U": cfg.U, "lmax": cfg.lmax,
+            "parity": "full" if cfg.full_parity else "natural", "paths": plan.n_paths, "cg_nnz": plan.nnz,
+        },
+        "kernel_ms": per_kernel_ms,
+        "step_event_ms": float(np.mean([ev[k][0].elapsed_time(ev[k][3]) for k in range(args.steps)])),
+        "hbm_algorithmic_GBps": {nm: algo[nm] / (per_kernel_ms[nm] / 1e3) / 1e9 for nm in names},
+        "copy_GBps_measured": copy_gbps,
+        "roofline": {
+            "kernel": "tp_backward",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": algo["tp_backward"],
+            "frac_of_measured_copy": achieved / copy_gbps,
+        },
+        "kernel_source_digest": kernel_source_digest(),
+    }
+    del x, w, g, out, grads, env
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        cfg_ = cfg
+
+        def host_inputs(e):
+            if cfg_.host_features:
+                return xh[:e], wh[:e], pwh, gh[:e]
+            xs, ws, gs = workloads.device_features(cfg_, n_edges, dev)
+            res = xs[:e].cpu().numpy(), ws[:e].cpu().numpy(), workloads.path_weights(cfg_), gs[:e].cpu().numpy()
+            del xs, ws, gs
+            torch.cuda.empty_cache()
+            return res
+
+        result["cpu_baseline"] = cpu_baseline(graph, host_inputs)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,216 @@
+"""ctypes binding of liballegro_tp.so -- argument marshalling only.
+
+Every function here has the name of the C entry point it calls (declared in
+include/allegro_tp.h), checks tensor shapes, dtypes, devices and contiguity,
+allocates outputs with PyTorch when the caller passes none, and hands raw
+device pointers plus the current HIP stream to the library.  No arithmetic of
+the operation happens in Python, and there is no fallback: if the compiled
+library is missing, importing this module raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liballegro_tp.so")
+
+ALLEGRO_OK = 0
+ALLEGRO_E_INVALID = -1
+ALLEGRO_E_UNSUPPORTED = -2
+ALLEGRO_E_HIP = -3
+ALLEGRO_E_NOMEM = -4
+ALLEGRO_FULL_PARITY = 1
+ALLEGRO_DETERMINISTIC = 2
+ALLEGRO_VALIDATE = 4
+
+EXPORTED = (
+    "allegro_tp_plan_create", "allegro_tp_plan_destroy", "allegro_tp_plan_query", "allegro_tp_plan_cg",
+    "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_last_error",
+)
+
+
+class AllegroError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"[{code}] {message}")
+        self.code = code
+
+
+def _load() -> ctypes.CDLL:
+    # PyTorch ships its own HIP runtime with the same soname as /opt/rocm's.
+    # Loading torch first makes the library bind to that one runtime; loading
+    # the library first would put two HIP runtimes in the process.
+    import torch  # noqa: F401
+
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2504_16068_amd.build.build() or "
+                          "__graft_entry__.build() first (there is no CPU fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    ip = ctypes.POINTER(ctypes.c_int)
+    lib.allegro_tp_plan_create.argtypes = [ctypes.POINTER(vp), i32, i32, i32]
+    lib.allegro_tp_plan_destroy.argtypes = [vp]
+    lib.allegro_tp_plan_query.argtypes = [vp, ip, ip, ip, ip, ip]
+    lib.allegro_tp_plan_cg.argtypes = [vp, ip, ctypes.POINTER(ctypes.c_double)]
+    lib.allegro_env_embed.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp]
+    lib.allegro_tp_forward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp]
+    lib.allegro_tp_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.allegro_last_error.restype = ctypes.c_char_p
+    for name in EXPORTED:
+        if name != "allegro_last_error":
+            getattr(lib, name).restype = i32
+    return lib
+
+
+_lib = _load()
+
+
+def library() -> ctypes.CDLL:
+    return _lib
+
+
+def allegro_last_error() -> str:
+    return _lib.allegro_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != ALLEGRO_OK:
+        raise AllegroError(rc, allegro_last_error())
+
+
+class Plan:
+    """Owns an allegro_tp_plan*; sizes are read back from the library."""
+
+    def __init__(self, handle: int, lmax: int, U: int, flags: int):
+        self.handle = ctypes.c_void_p(handle)
+        self.lmax, self.U, self.flags = lmax, U, flags
+        d1, d2, np_, nnz = (ctypes.c_int() for _ in range(4))
+        _check(_lib.allegro_tp_plan_query(self.handle, ctypes.byref(d1), ctypes.byref(d2), ctypes.byref(np_), None,
+                                          ctypes.byref(nnz)))
+        self.d1, self.d2, self.n_paths, self.nnz = d1.value, d2.value, np_.value, nnz.value
+
+    def path_desc(self):
+        buf = (ctypes.c_int * (6 * self.n_paths))()
+        _check(_lib.allegro_tp_plan_query(self.handle, None, None, None, buf, None))
+        return [tuple(buf[6 * p:6 * p + 6]) for p in range(self.n_paths)]
+
+    def cg_table(self):
+        """(list of (path, i, j, k), list of coefficients) of the sparse combined table."""
+        idx = (ctypes.c_int * (4 * self.nnz))()
+        val = (ctypes.c_double * self.nnz)()
+        _check(_lib.allegro_tp_plan_cg(self.handle, idx, val))
+        return [tuple(idx[4 * q:4 * q + 4]) for q in range(self.nnz)], list(val)
+
+    def close(self):
+        if self.handle is not None and self.handle.value:
+            _lib.allegro_tp_plan_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def allegro_tp_plan_create(lmax: int, U: int, flags: int = ALLEGRO_FULL_PARITY) -> Plan:
+    h = ctypes.c_void_p()
+    _check(_lib.allegro_tp_plan_create(ctypes.byref(h), int(lmax), int(U), int(flags)))
+    return Plan(h.value, lmax, U, flags)
+
+
+def allegro_tp_plan_destroy(plan: Plan):
+    plan.close()
+
+
+# ----------------------------------------------------------------- tensors
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
+
+
+def _need(t, name, shape, dtype, device):
+    import torch
+
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device != device or t.device.type != "cuda":
+        raise ValueError(f"{name} must live on {device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(stream, device):
+    import torch
+
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _sizes(plan: Plan, row_ptr, n_edges):
+    import torch
+
+    if row_ptr.dtype != torch.int64 or row_ptr.dim() != 1 or not row_ptr.is_contiguous():
+        raise ValueError("row_ptr must be a contiguous 1-D int64 tensor")
+    return row_ptr.numel() - 1, n_edges
+
+
+def allegro_env_embed(plan: Plan, row_ptr, w, Y, env=None, stream=None):
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, w.shape[0])
+    _need(w, "w", (e, plan.U), torch.float32, dev)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    if env is None:
+        env = torch.empty((n, plan.U, plan.d2), device=dev, dtype=torch.float32)
+    _need(env, "env", (n, plan.U, plan.d2), torch.float32, dev)
+    _check(_lib.allegro_env_embed(plan.handle, n, e, _ptr(row_ptr), _ptr(w), _ptr(Y), _ptr(env),
+                                  _stream(stream, dev)))
+    return env
+
+
+def allegro_tp_forward(plan: Plan, row_ptr, x, env, path_w, out=None, stream=None):
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, x.shape[0])
+    _need(x, "x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(env, "env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(path_w, "path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    if out is None:
+        out = torch.empty_like(x)
+    _need(out, "out", (e, plan.U, plan.d1), torch.float32, dev)
+    _check(_lib.allegro_tp_forward(plan.handle, n, e, _ptr(row_ptr), _ptr(x), _ptr(env), _ptr(path_w), _ptr(out),
+                                   _stream(stream, dev)))
+    return out
+
+
+def allegro_tp_backward(plan: Plan, row_ptr, x, env, path_w, grad_out, w, Y, outs=None, stream=None):
+    """Returns (grad_x, grad_env, grad_w, grad_Y)."""
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, x.shape[0])
+    _need(x, "x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(env, "env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(path_w, "path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    _need(grad_out, "grad_out", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(w, "w", (e, plan.U), torch.float32, dev)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    if outs is None:
+        outs = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(Y))
+    gx, genv, gw, gy = outs
+    _need(gx, "grad_x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(genv, "grad_env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(gw, "grad_w", (e, plan.U), torch.float32, dev)
+    _need(gy, "grad_Y", (e, plan.d2), torch.float32, dev)
+    _check(_lib.allegro_tp_backward(plan.handle, n, e, _ptr(row_ptr), _ptr(x), _ptr(env), _ptr(path_w),
+                                    _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw), _ptr(gy),
+                                    _stream(stream, dev)))
+    return gx, genv, gw, gy

@@ -1,0 +1,507 @@
+// MI355X (gfx950) kernels and C ABI of the Allegro channel-wise tensor product.
+//
+// What is computed is stated in include/allegro_tp.h (arxiv 2504.16068, §II.D:
+// the tensor product, its first derivative, and the embedding it consumes).
+//
+// Mapping (wave64, one 64-lane workgroup per center atom):
+//   * lane <-> channel u.  With U < 64 a wave holds 64/U lane groups that take
+//     every (64/U)-th edge of the segment; with U = 128 each lane owns two
+//     channels, processed one after the other.
+//   * Path weights W[:, u] and env[n, u, :] are loaded once per center into
+//     VGPRs; every edge then streams x (and g) from HBM and the contraction
+//     runs in registers with the coupling coefficients as instruction
+//     literals (generated cores, tp_cores.inc).
+//   * Segment ownership: a center's workgroup owns its env / grad_env rows, so
+//     every segmented reduction is a fixed-order register accumulation -- no
+//     atomics, bit-identical from run to run.
+//   * The embedding VJP (grad_w, grad_Y) reruns the segment with lane <-> edge:
+//     grad_env of the center is staged in LDS and read as wave-uniform
+//     broadcasts, so the sum over channels for grad_Y needs no cross-lane
+//     reduction.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "allegro_tp.h"
+#include "cg_builder.hpp"
+#include "generated/tp_cores.inc"
+
+namespace {
+
+constexpr int kWave = 64;
+
+template <int U>
+struct Lanes {
+  static_assert(U == 16 || U == 32 || U == 64 || U == 128, "U must be 16, 32, 64 or 128");
+  static constexpr int LPE = U < kWave ? U : kWave;  // lanes per edge group
+  static constexpr int G = kWave / LPE;              // edge groups per wave
+  static constexpr int CPL = U / LPE;                // channels per lane
+};
+
+// ----------------------------------------------------------------- vector I/O
+// Per-lane contiguous rows of D floats; the row start is 4*D-byte aligned
+// relative to a 16-byte aligned base, so the widest aligned access is used.
+template <int D>
+__device__ __forceinline__ void load_row(const float *__restrict__ p, float (&r)[D]) {
+  if constexpr (D % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i) {
+      const float4 v = reinterpret_cast<const float4 *>(p)[i];
+      r[4 * i] = v.x; r[4 * i + 1] = v.y; r[4 * i + 2] = v.z; r[4 * i + 3] = v.w;
+    }
+  } else if constexpr (D % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) {
+      const float2 v = reinterpret_cast<const float2 *>(p)[i];
+      r[2 * i] = v.x; r[2 * i + 1] = v.y;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < D; ++i) r[i] = p[i];
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void store_row(float *__restrict__ p, const float (&r)[D]) {
+  if constexpr (D % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < D / 4; ++i)
+      reinterpret_cast<float4 *>(p)[i] = make_float4(r[4 * i], r[4 * i + 1], r[4 * i + 2], r[4 * i + 3]);
+  } else if constexpr (D % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < D / 2; ++i) reinterpret_cast<float2 *>(p)[i] = make_float2(r[2 * i], r[2 * i + 1]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < D; ++i) p[i] = r[i];
+  }
+}
+
+// acc + fl(a * b) with two separate roundings (no contraction to FMA).
+__device__ __forceinline__ float add_rounded_product(float acc, float a, float b) {
+#pragma clang fp contract(off)
+  const float prod = a * b;
+  return acc + prod;
+}
+
+// ------------------------------------------------------------ env embedding
+// env[n,u,j] = sum_{e in seg(n)} w[e,u] Y[e,j].  Lane groups take different
+// centers (U < 64) so every env value is one lane's ascending-e sum.
+template <int U, int D2, bool DET>
+__global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64_t *__restrict__ row_ptr,
+                                                          const float *__restrict__ w,
+                                                          const float *__restrict__ Y, float *__restrict__ env) {
+  using L = Lanes<U>;
+  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int64_t n = int64_t(blockIdx.x) * L::G + grp;
+  if (n >= N) return;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  float acc[L::CPL][D2];
+#pragma unroll
+  for (int t = 0; t < L::CPL; ++t)
+#pragma unroll
+    for (int j = 0; j < D2; ++j) acc[t][j] = 0.0f;
+  for (int64_t e = e0; e < e1; ++e) {
+    float y[D2];
+#pragma unroll
+    for (int j = 0; j < D2; ++j) y[j] = Y[e * D2 + j];
+#pragma unroll
+    for (int t = 0; t < L::CPL; ++t) {
+      const float wv = w[e * U + ul + t * kWave];
+#pragma unroll
+      for (int j = 0; j < D2; ++j)
+        acc[t][j] = DET ? add_rounded_product(acc[t][j], wv, y[j]) : __builtin_fmaf(wv, y[j], acc[t][j]);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
+}
+
+// ------------------------------------------------------ tensor product fwd
+template <class Core, int U>
+__global__ __launch_bounds__(kWave) void tp_forward_kernel(const int64_t *__restrict__ row_ptr,
+                                                           const float *__restrict__ x,
+                                                           const float *__restrict__ env,
+                                                           const float *__restrict__ path_w,
+                                                           float *__restrict__ out) {
+  using L = Lanes<U>;
+  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP;
+  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int64_t n = blockIdx.x;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+#pragma unroll 1
+  for (int t = 0; t < L::CPL; ++t) {
+    const int u = ul + t * kWave;
+    float wr[NP], er[D2];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) wr[p] = path_w[p * U + u];
+    load_row<D2>(env + (n * U + u) * D2, er);
+    for (int64_t e = e0 + grp; e < e1; e += L::G) {
+      float xr[D1], orow[D1];
+      load_row<D1>(x + (e * U + u) * D1, xr);
+      Core::fwd(xr, er, wr, orow);
+      store_row<D1>(out + (e * U + u) * D1, orow);
+    }
+  }
+}
+
+// ------------------------------------------------------ tensor product bwd
+template <class Core, int U>
+__global__ __launch_bounds__(kWave) void tp_backward_kernel(
+    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+    const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
+    const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
+    float *__restrict__ grad_w, float *__restrict__ grad_Y) {
+  using L = Lanes<U>;
+  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP;
+  __shared__ float ge_s[U * D2];                  // grad_env[n, :, :] of this center
+  __shared__ float part_s[L::G > 1 ? kWave * D2 : 1];  // per-group partial sums (U < 64)
+  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int64_t n = blockIdx.x;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+
+  // Pass 1 (lane <-> channel): grad_x per edge, grad_env accumulated in registers.
+#pragma unroll 1
+  for (int t = 0; t < L::CPL; ++t) {
+    const int u = ul + t * kWave;
+    float wr[NP], er[D2], ge[D2];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) wr[p] = path_w[p * U + u];
+    load_row<D2>(env + (n * U + u) * D2, er);
+#pragma unroll
+    for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
+    for (int64_t e = e0 + grp; e < e1; e += L::G) {
+      float xr[D1], gr[D1], gxr[D1];
+      load_row<D1>(x + (e * U + u) * D1, xr);
+      load_row<D1>(g + (e * U + u) * D1, gr);
+      Core::bwd(xr, er, wr, gr, gxr, ge);
+      store_row<D1>(grad_x + (e * U + u) * D1, gxr);
+    }
+    if constexpr (L::G == 1) {
+#pragma unroll
+      for (int j = 0; j < D2; ++j) ge_s[u * D2 + j] = ge[j];
+    } else {
+      // combine the lane groups in a fixed order
+#pragma unroll
+      for (int j = 0; j < D2; ++j) part_s[lane * D2 + j] = ge[j];
+      __syncthreads();
+      if (grp == 0) {
+#pragma unroll
+        for (int j = 0; j < D2; ++j) {
+          float s = part_s[ul * D2 + j];
+          for (int q = 1; q < L::G; ++q) s += part_s[(q * L::LPE + ul) * D2 + j];
+          ge_s[u * D2 + j] = s;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  for (int i = lane; i < U * D2; i += kWave) grad_env[n * U * D2 + i] = ge_s[i];
+
+  // Pass 2 (lane <-> edge): grad_w[e,u] = sum_j ge[u,j] Y[e,j], grad_Y[e,j] = sum_u ge[u,j] w[e,u].
+  for (int64_t e = e0 + lane; e < e1; e += kWave) {
+    float y[D2], gy[D2];
+    load_row<D2>(Y + e * D2, y);
+#pragma unroll
+    for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
+#pragma unroll 1
+    for (int u0 = 0; u0 < U; u0 += 4) {
+      float wv[4], gw[4];
+      load_row<4>(w + e * U + u0, wv);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D2; ++j) {
+          const float gej = ge_s[(u0 + c) * D2 + j];
+          acc = __builtin_fmaf(gej, y[j], acc);
+          gy[j] = __builtin_fmaf(gej, wv[c], gy[j]);
+        }
+        gw[c] = acc;
+      }
+      store_row<4>(grad_w + e * U + u0, gw);
+    }
+    store_row<D2>(grad_Y + e * D2, gy);
+  }
+}
+
+// ------------------------------------------------------------- CSR check
+__global__ void zero_word_kernel(int *word) { *word = 0; }
+
+__global__ void csr_check_kernel(int64_t N, int64_t E, const int64_t *__restrict__ row_ptr, int *status) {
+  const int64_t stride = int64_t(gridDim.x) * blockDim.x;
+  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i <= N; i += stride) {
+    const int64_t v = row_ptr[i];
+    bool bad = v < 0 || v > E;
+    if (i == 0 && v != 0) bad = true;
+    if (i == N && v != E) bad = true;
+    if (i < N && row_ptr[i + 1] < v) bad = true;
+    if (bad) atomicOr(status, 1);
+  }
+}
+
+// ------------------------------------------------------------- host side
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+}  // namespace
+
+struct allegro_tp_plan {
+  int lmax = 0, U = 0, flags = 0;
+  allegro::TPTable table;
+  int *status = nullptr;  // device word for ALLEGRO_VALIDATE
+  std::mutex validate_mu;
+};
+
+namespace {
+
+using EnvFn = void (*)(dim3, hipStream_t, int64_t, const int64_t *, const float *, const float *, float *);
+using FwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, float *);
+using BwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, const float *,
+                       const float *, const float *, float *, float *, float *, float *);
+
+template <int U, int D2, bool DET>
+void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const float *w, const float *Y, float *env) {
+  hipLaunchKernelGGL((env_embed_kernel<U, D2, DET>), grid, dim3(kWave), 0, s, N, rp, w, Y, env);
+}
+
+template <class Core, int U>
+void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
+                float *out) {
+  hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave), 0, s, rp, x, env, pw, out);
+}
+
+template <class Core, int U>
+void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
+                const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy) {
+  hipLaunchKernelGGL((tp_backward_kernel<Core, U>), grid, dim3(kWave), 0, s, rp, x, env, pw, g, w, Y, gx, genv, gw,
+                     gy);
+}
+
+struct Kernels {
+  EnvFn env = nullptr;
+  FwdFn fwd = nullptr;
+  BwdFn bwd = nullptr;
+};
+
+template <int LMAX, bool FULL, int U>
+Kernels kernels_for(bool det) {
+  using Core = TPCore<LMAX, FULL>;
+  Kernels k;
+  k.env = det ? &launch_env<U, Core::D2, true> : &launch_env<U, Core::D2, false>;
+  k.fwd = &launch_fwd<Core, U>;
+  k.bwd = &launch_bwd<Core, U>;
+  return k;
+}
+
+template <int LMAX, bool FULL>
+Kernels kernels_for_u(int U, bool det) {
+  switch (U) {
+    case 16: return kernels_for<LMAX, FULL, 16>(det);
+    case 32: return kernels_for<LMAX, FULL, 32>(det);
+    case 64: return kernels_for<LMAX, FULL, 64>(det);
+    case 128: return kernels_for<LMAX, FULL, 128>(det);
+    default: return {};
+  }
+}
+
+Kernels select(const allegro_tp_plan *p) {
+  const bool full = (p->flags & ALLEGRO_FULL_PARITY) != 0, det = (p->flags & ALLEGRO_DETERMINISTIC) != 0;
+  switch (p->lmax * 2 + (full ? 1 : 0)) {
+    case 2: return kernels_for_u<1, false>(p->U, det);
+    case 3: return kernels_for_u<1, true>(p->U, det);
+    case 4: return kernels_for_u<2, false>(p->U, det);
+    case 5: return kernels_for_u<2, true>(p->U, det);
+    case 6: return kernels_for_u<3, false>(p->U, det);
+    case 7: return kernels_for_u<3, true>(p->U, det);
+    default: return {};
+  }
+}
+
+int check_sizes(const allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_ptr) {
+  if (!p) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (N < 0 || E < 0) return fail(ALLEGRO_E_INVALID, "negative size (N=%lld, E=%lld)", (long long)N, (long long)E);
+  if (N == 0 && E > 0) return fail(ALLEGRO_E_INVALID, "E=%lld edges but N=0 centers", (long long)E);
+  if (N >= (int64_t(1) << 31)) return fail(ALLEGRO_E_INVALID, "N=%lld exceeds 2^31-1", (long long)N);
+  if (N > 0 && !row_ptr) return fail(ALLEGRO_E_INVALID, "row_ptr is NULL");
+  if (row_ptr && (reinterpret_cast<uintptr_t>(row_ptr) & 7u))
+    return fail(ALLEGRO_E_INVALID, "row_ptr is not 8-byte aligned");
+  return ALLEGRO_OK;
+}
+
+int check_tensor(const void *ptr, const char *name) {
+  if (!ptr) return fail(ALLEGRO_E_INVALID, "%s is NULL", name);
+  if (misaligned(ptr)) return fail(ALLEGRO_E_INVALID, "%s is not 16-byte aligned", name);
+  return ALLEGRO_OK;
+}
+
+int validate_csr(allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_ptr, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(p->validate_mu);
+  hipLaunchKernelGGL(zero_word_kernel, dim3(1), dim3(1), 0, s, p->status);
+  const int64_t blocks = std::min<int64_t>((N + 256) / 256, 4096);
+  hipLaunchKernelGGL(csr_check_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, N, E, row_ptr, p->status);
+  int host = 0;
+  if (hipMemcpyAsync(&host, p->status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(ALLEGRO_E_HIP, "CSR validation failed to run: %s", hipGetErrorString(hipGetLastError()));
+  if (host) return fail(ALLEGRO_E_INVALID, "row_ptr is not a valid CSR pointer for N=%lld, E=%lld", (long long)N,
+                        (long long)E);
+  return ALLEGRO_OK;
+}
+
+int after_launch(const char *what) {
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(ALLEGRO_E_HIP, "%s launch failed: %s", what, hipGetErrorString(err));
+  return ALLEGRO_OK;
+}
+
+// Blocks of 64 lanes: the env kernel packs 64/U centers per block when U < 64.
+unsigned env_blocks(int U, int64_t N) {
+  const int per = U < kWave ? kWave / U : 1;
+  return unsigned((N + per - 1) / per);
+}
+
+}  // namespace
+
+extern "C" {
+
+int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan output pointer is NULL");
+  *plan = nullptr;
+  if (lmax < 1 || lmax > 3) return fail(ALLEGRO_E_UNSUPPORTED, "lmax=%d not supported (1, 2 or 3)", lmax);
+  if (U != 16 && U != 32 && U != 64 && U != 128)
+    return fail(ALLEGRO_E_UNSUPPORTED, "U=%d not supported (16, 32, 64 or 128)", U);
+  if (flags & ~(ALLEGRO_FULL_PARITY | ALLEGRO_DETERMINISTIC | ALLEGRO_VALIDATE))
+    return fail(ALLEGRO_E_INVALID, "unknown flags 0x%x", flags);
+  allegro_tp_plan *p = new (std::nothrow) allegro_tp_plan;
+  if (!p) return fail(ALLEGRO_E_NOMEM, "plan allocation failed");
+  p->lmax = lmax;
+  p->U = U;
+  p->flags = flags;
+  try {
+    p->table = allegro::build_table(lmax, (flags & ALLEGRO_FULL_PARITY) != 0);
+  } catch (const std::exception &ex) {
+    delete p;
+    return fail(ALLEGRO_E_INVALID, "coupling table build failed: %s", ex.what());
+  }
+  if ((flags & ALLEGRO_VALIDATE) && hipMalloc(&p->status, sizeof(int)) != hipSuccess) {
+    delete p;
+    return fail(ALLEGRO_E_NOMEM, "device status word allocation failed: %s", hipGetErrorString(hipGetLastError()));
+  }
+  *plan = p;
+  return ALLEGRO_OK;
+}
+
+int allegro_tp_plan_destroy(allegro_tp_plan *plan) {
+  if (!plan) return ALLEGRO_OK;
+  if (plan->status) (void)hipFree(plan->status);
+  delete plan;
+  return ALLEGRO_OK;
+}
+
+int allegro_tp_plan_query(const allegro_tp_plan *plan, int *d1, int *d2, int *n_paths, int *path_desc, int *nnz) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  const auto &t = plan->table;
+  if (d1) *d1 = t.d1;
+  if (d2) *d2 = t.d2;
+  if (n_paths) *n_paths = int(t.paths.size());
+  if (nnz) *nnz = int(t.entries.size());
+  if (path_desc)
+    for (size_t p = 0; p < t.paths.size(); ++p) {
+      const auto &ph = t.paths[p];
+      const int row[6] = {t.x_irreps[ph.a].l, t.x_irreps[ph.a].p, t.env_irreps[ph.b].l,
+                          t.env_irreps[ph.b].p, t.x_irreps[ph.c].l, t.x_irreps[ph.c].p};
+      std::memcpy(path_desc + 6 * p, row, sizeof row);
+    }
+  return ALLEGRO_OK;
+}
+
+int allegro_tp_plan_cg(const allegro_tp_plan *plan, int *idx, double *val) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (!idx || !val) return fail(ALLEGRO_E_INVALID, "output array is NULL");
+  const auto &es = plan->table.entries;
+  for (size_t q = 0; q < es.size(); ++q) {
+    idx[4 * q] = es[q].path;
+    idx[4 * q + 1] = es[q].i;
+    idx[4 * q + 2] = es[q].j;
+    idx[4 * q + 3] = es[q].k;
+    val[q] = es[q].value;
+  }
+  return ALLEGRO_OK;
+}
+
+int allegro_env_embed(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr, const float *w,
+                      const float *Y, float *env, void *stream) {
+  int rc = check_sizes(plan, N, E, row_ptr);
+  if (rc) return rc;
+  if (N == 0) return ALLEGRO_OK;
+  if ((rc = check_tensor(env, "env"))) return rc;
+  if (E > 0 && ((rc = check_tensor(w, "w")) || (rc = check_tensor(Y, "Y")))) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto *mp = const_cast<allegro_tp_plan *>(plan);
+  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const Kernels k = select(plan);
+  if (!k.env) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  k.env(dim3(env_blocks(plan->U, N)), s, N, row_ptr, w, Y, env);
+  return after_launch("allegro_env_embed");
+}
+
+int allegro_tp_forward(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr, const float *x,
+                       const float *env, const float *path_w, float *out, void *stream) {
+  int rc = check_sizes(plan, N, E, row_ptr);
+  if (rc) return rc;
+  if (E == 0) return ALLEGRO_OK;
+  if ((rc = check_tensor(x, "x")) || (rc = check_tensor(env, "env")) || (rc = check_tensor(path_w, "path_w")) ||
+      (rc = check_tensor(out, "out")))
+    return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto *mp = const_cast<allegro_tp_plan *>(plan);
+  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const Kernels k = select(plan);
+  if (!k.fwd) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  k.fwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, out);
+  return after_launch("allegro_tp_forward");
+}
+
+int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr, const float *x,
+                        const float *env, const float *path_w, const float *grad_out, const float *w, const float *Y,
+                        float *grad_x, float *grad_env, float *grad_w, float *grad_Y, void *stream) {
+  int rc = check_sizes(plan, N, E, row_ptr);
+  if (rc) return rc;
+  if (N == 0) return ALLEGRO_OK;
+  if ((rc = check_tensor(grad_env, "grad_env")) || (rc = check_tensor(env, "env")) ||
+      (rc = check_tensor(path_w, "path_w")))
+    return rc;
+  if (E > 0 && ((rc = check_tensor(x, "x")) || (rc = check_tensor(grad_out, "grad_out")) ||
+                (rc = check_tensor(w, "w")) || (rc = check_tensor(Y, "Y")) || (rc = check_tensor(grad_x, "grad_x")) ||
+                (rc = check_tensor(grad_w, "grad_w")) || (rc = check_tensor(grad_Y, "grad_Y"))))
+    return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  auto *mp = const_cast<allegro_tp_plan *>(plan);
+  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const Kernels k = select(plan);
+  if (!k.bwd) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y);
+  return after_launch("allegro_tp_backward");
+}
+
+const char *allegro_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,182 @@
+// Build-time generator: writes the register-resident contraction cores of the
+// tensor product for every supported (lmax, parity mode) as straight-line HIP
+// device code, from the sparse combined coupling table of cg_builder.
+//
+// Every coefficient becomes an fp32 literal and every register index a
+// compile-time constant, so the per-lane operands stay in VGPRs and the
+// coupling table costs no memory traffic at all.  The generated cores are
+//   fwd: out[k]  = sum_p W[p] sum_{(i,j,k) in p} C q_ij,  q_ij = x[i] env[j]
+//        (products shared by all paths with the same input blocks (a, b))
+//   bwd: Q_ij    = sum_{p with blocks (a,b)} sum_k C (W[p] g[k])
+//        gx[i]   = sum_j Q_ij env[j]           (overwritten)
+//        ge[j]  += sum_i Q_ij x[i]             (accumulated across edges)
+// which is the tensor product and its VJP with respect to x and env, written
+// per pair of input blocks so that at most one block of temporaries is live.
+//
+// Usage: gen_kernels <output.inc>
+#include <cstdio>
+#include <map>
+#include <set>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "cg_builder.hpp"
+
+namespace {
+
+std::string lit(double v) {
+  char buf[64];
+  std::snprintf(buf, sizeof buf, "%af", double(float(v)));
+  return buf;
+}
+
+struct Group {  // all paths that share the input blocks (a, b)
+  int a, b;
+  std::vector<int> paths;
+};
+
+std::vector<Group> groups_of(const allegro::TPTable &t) {
+  std::vector<Group> gs;
+  for (int p = 0; p < int(t.paths.size()); ++p) {
+    const auto &ph = t.paths[p];
+    if (gs.empty() || gs.back().a != ph.a || gs.back().b != ph.b) gs.push_back({ph.a, ph.b, {}});
+    gs.back().paths.push_back(p);
+  }
+  return gs;
+}
+
+// "acc = acc + c * term" with the first assignment and +-1 coefficients folded.
+std::string accumulate(const std::string &acc, bool first, double c, const std::string &term) {
+  const float cf = float(c);
+  if (first) {
+    if (cf == 1.0f) return acc + " = " + term + ";";
+    if (cf == -1.0f) return acc + " = -" + term + ";";
+    return acc + " = " + lit(c) + " * " + term + ";";
+  }
+  if (cf == 1.0f) return acc + " = " + acc + " + " + term + ";";
+  if (cf == -1.0f) return acc + " = " + acc + " - " + term + ";";
+  return acc + " = __builtin_fmaf(" + lit(c) + ", " + term + ", " + acc + ");";
+}
+
+void emit_core(FILE *f, const allegro::TPTable &t) {
+  const int np = int(t.paths.size());
+  std::fprintf(f, "template <> struct TPCore<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
+  std::fprintf(f, "  static constexpr int LMAX = %d, D1 = %d, D2 = %d, NP = %d, NNZ = %d;\n", t.lmax, t.d1, t.d2, np,
+               int(t.entries.size()));
+
+  // entries grouped per path
+  std::vector<std::vector<allegro::CGEntry>> per_path(np);
+  for (const auto &e : t.entries) per_path[e.path].push_back(e);
+  const auto groups = groups_of(t);
+
+  // ---------------------------------------------------------------- forward
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void fwd(const float *__restrict__ x, const float *__restrict__ env,\n"
+               "                                             const float *__restrict__ W, float *__restrict__ out) {\n");
+  std::vector<bool> out_init(t.d1, false);
+  for (const Group &g : groups) {
+    std::fprintf(f, "    { // x block %d (l=%d) with env block %d (l=%d)\n", g.a, t.x_irreps[g.a].l, g.b,
+                 t.env_irreps[g.b].l);
+    std::set<std::pair<int, int>> pairs;
+    for (int p : g.paths)
+      for (const auto &e : per_path[p]) pairs.insert({e.i, e.j});
+    for (const auto &ij : pairs)
+      std::fprintf(f, "      const float q%d_%d = x[%d] * env[%d];\n", ij.first, ij.second, ij.first, ij.second);
+    for (int p : g.paths) {
+      std::map<int, std::vector<allegro::CGEntry>> by_k;
+      for (const auto &e : per_path[p]) by_k[e.k].push_back(e);
+      for (const auto &kv : by_k) {
+        std::fprintf(f, "      { float s;");
+        bool first = true;
+        for (const auto &e : kv.second) {
+          std::fprintf(f, " %s", accumulate("s", first, e.value, "q" + std::to_string(e.i) + "_" + std::to_string(e.j)).c_str());
+          first = false;
+        }
+        const int k = kv.first;
+        if (out_init[k])
+          std::fprintf(f, " out[%d] = __builtin_fmaf(W[%d], s, out[%d]); }\n", k, p, k);
+        else
+          std::fprintf(f, " out[%d] = W[%d] * s; }\n", k, p);
+        out_init[k] = true;
+      }
+    }
+    std::fprintf(f, "    }\n");
+  }
+  for (int k = 0; k < t.d1; ++k)
+    if (!out_init[k]) std::fprintf(f, "    out[%d] = 0.0f;\n", k);
+  std::fprintf(f, "  }\n");
+
+  // ---------------------------------------------------------------- backward
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void bwd(const float *__restrict__ x, const float *__restrict__ env,\n"
+               "                                             const float *__restrict__ W, const float *__restrict__ g,\n"
+               "                                             float *__restrict__ gx, float *__restrict__ ge) {\n");
+  std::vector<bool> gx_init(t.d1, false);
+  for (const Group &g : groups) {
+    std::fprintf(f, "    { // x block %d with env block %d\n", g.a, g.b);
+    std::set<std::pair<int, int>> wg_needed;  // (path, k)
+    for (int p : g.paths)
+      for (const auto &e : per_path[p]) wg_needed.insert({p, e.k});
+    for (const auto &pk : wg_needed)
+      std::fprintf(f, "      const float wg%d_%d = W[%d] * g[%d];\n", pk.first, pk.second, pk.first, pk.second);
+    std::map<std::pair<int, int>, bool> q_init;
+    std::vector<std::pair<int, int>> q_order;
+    for (int p : g.paths)
+      for (const auto &e : per_path[p]) {
+        const auto ij = std::make_pair(e.i, e.j);
+        const bool first = !q_init.count(ij);
+        const std::string name = "Q" + std::to_string(e.i) + "_" + std::to_string(e.j);
+        if (first) {
+          q_order.push_back(ij);
+          q_init[ij] = true;
+          std::fprintf(f, "      float %s;", name.c_str());
+        } else {
+          std::fprintf(f, "     ");
+        }
+        std::fprintf(f, " %s\n",
+                     accumulate(name, first, e.value, "wg" + std::to_string(p) + "_" + std::to_string(e.k)).c_str());
+      }
+    for (const auto &ij : q_order) {
+      const int i = ij.first, j = ij.second;
+      if (gx_init[i])
+        std::fprintf(f, "      gx[%d] = __builtin_fmaf(Q%d_%d, env[%d], gx[%d]);", i, i, j, j, i);
+      else
+        std::fprintf(f, "      gx[%d] = Q%d_%d * env[%d];", i, i, j, j);
+      gx_init[i] = true;
+      std::fprintf(f, " ge[%d] = __builtin_fmaf(Q%d_%d, x[%d], ge[%d]);\n", j, i, j, i, j);
+    }
+    std::fprintf(f, "    }\n");
+  }
+  for (int i = 0; i < t.d1; ++i)
+    if (!gx_init[i]) std::fprintf(f, "    gx[%d] = 0.0f;\n", i);
+  std::fprintf(f, "  }\n};\n\n");
+}
+
+}  // namespace
+
+int main(int argc, char **argv) {
+  if (argc != 2) {
+    std::fprintf(stderr, "usage: %s <output.inc>\n", argv[0]);
+    return 2;
+  }
+  FILE *f = std::fopen(argv[1], "w");
+  if (!f) {
+    std::perror(argv[1]);
+    return 1;
+  }
+  std::fprintf(f,
+               "// Generated by gen_kernels from the sparse coupling table of cg_builder. Do not edit.\n"
+               "#pragma once\n\n"
+               "template <int LMAX, bool FULL> struct TPCore;\n\n");
+  try {
+    for (int lmax = 1; lmax <= 3; ++lmax)
+      for (int full = 0; full <= 1; ++full) emit_core(f, allegro::build_table(lmax, full != 0));
+  } catch (const std::exception &ex) {
+    std::fprintf(stderr, "gen_kernels: %s\n", ex.what());
+    std::fclose(f);
+    return 1;
+  }
+  std::fclose(f);
+  return 0;
+}

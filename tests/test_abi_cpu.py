@@ -1,0 +1,123 @@
+"""Host-side tests of the C ABI (no GPU): exports, plans, coupling table, errors.
+
+The coupling table of the library comes from its own C++ builder (null space of
+the so(3) intertwiner equations); here it is compared, as outputs only, with
+the oracle's table (Racah's formula plus the change of basis).  Error paths are
+exercised only where the library rejects the call before any HIP call.
+"""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import cg as ocg
+from oracle import irreps as oirreps
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "allegro_tp.h")
+
+binding = pytest.importorskip("paper_2504_16068_amd.binding",
+                              reason="liballegro_tp.so not built (run __graft_entry__.build())")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(allegro_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.library()
+    names = _declared_functions()
+    assert set(names) == set(binding.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+CONFIGS = [(lmax, full, u) for lmax in (1, 2, 3) for full in (False, True) for u in (16, 32, 64, 128)]
+
+
+@pytest.mark.parametrize("lmax,full,U", CONFIGS)
+def test_plan_sizes_and_paths_match_oracle(lmax, full, U):
+    flags = binding.ALLEGRO_FULL_PARITY if full else 0
+    plan = binding.allegro_tp_plan_create(lmax, U, flags)
+    xs, es = oirreps.x_irreps(lmax, full), oirreps.env_irreps(lmax)
+    assert plan.d1 == oirreps.dim(xs) and plan.d2 == oirreps.dim(es)
+    ps = oirreps.paths(lmax, full)
+    assert plan.n_paths == len(ps)
+    expect = [(xs[a][0], xs[a][1], es[b][0], es[b][1], xs[c][0], xs[c][1]) for a, b, c in ps]
+    assert plan.path_desc() == expect
+    plan.close()
+
+
+@pytest.mark.parametrize("lmax,full", [(1, False), (1, True), (2, False), (2, True), (3, False), (3, True)])
+def test_coupling_table_matches_oracle(lmax, full):
+    plan = binding.allegro_tp_plan_create(lmax, 64, binding.ALLEGRO_FULL_PARITY if full else 0)
+    idx, val = plan.cg_table()
+    ref = ocg.combined_sparse(lmax, full)
+    assert plan.nnz == len(ref) == len(idx)
+    got = {k: v for k, v in zip(idx, val)}
+    want = {(p, i, j, k): v for p, i, j, k, v in ref}
+    assert set(got) == set(want)
+    err = max(abs(got[k] - want[k]) for k in want)
+    assert err <= 1e-14, err
+
+
+def _err(fn, *args):
+    rc = fn(*args)
+    return rc, binding.allegro_last_error()
+
+
+def test_plan_create_rejects_bad_arguments():
+    lib = binding.library()
+    h = ctypes.c_void_p()
+    rc, msg = _err(lib.allegro_tp_plan_create, ctypes.byref(h), 4, 64, 1)
+    assert rc == binding.ALLEGRO_E_UNSUPPORTED and "lmax" in msg and not h.value
+    rc, msg = _err(lib.allegro_tp_plan_create, ctypes.byref(h), 2, 48, 1)
+    assert rc == binding.ALLEGRO_E_UNSUPPORTED and "U=48" in msg
+    rc, msg = _err(lib.allegro_tp_plan_create, ctypes.byref(h), 2, 64, 64)
+    assert rc == binding.ALLEGRO_E_INVALID and "flags" in msg
+    rc, _ = _err(lib.allegro_tp_plan_create, None, 2, 64, 1)
+    assert rc == binding.ALLEGRO_E_INVALID
+    with pytest.raises(binding.AllegroError) as ex:
+        binding.allegro_tp_plan_create(0, 64)
+    assert ex.value.code == binding.ALLEGRO_E_UNSUPPORTED
+    assert lib.allegro_tp_plan_destroy(None) == binding.ALLEGRO_OK
+
+
+def test_entry_points_reject_bad_arguments_before_any_launch():
+    lib = binding.library()
+    plan = binding.allegro_tp_plan_create(2, 64, binding.ALLEGRO_FULL_PARITY)
+    h = plan.handle
+    vp = ctypes.c_void_p
+    ok_ptr, ok_rp, bad_ptr = vp(0x10000), vp(0x20000), vp(0x10004)
+    # null plan
+    rc, msg = _err(lib.allegro_env_embed, None, 1, 1, ok_rp, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "plan" in msg
+    # negative sizes, edges without centers, huge N
+    rc, msg = _err(lib.allegro_tp_forward, h, -1, 5, ok_rp, ok_ptr, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "negative" in msg
+    rc, msg = _err(lib.allegro_tp_forward, h, 0, 5, ok_rp, ok_ptr, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "N=0" in msg
+    rc, msg = _err(lib.allegro_tp_forward, h, 1 << 31, 5, ok_rp, ok_ptr, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "2^31" in msg
+    # null / misaligned tensors
+    rc, msg = _err(lib.allegro_tp_forward, h, 3, 5, ok_rp, None, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "x is NULL" in msg
+    rc, msg = _err(lib.allegro_tp_forward, h, 3, 5, ok_rp, bad_ptr, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "aligned" in msg
+    rc, msg = _err(lib.allegro_tp_forward, h, 3, 5, vp(0x20004), ok_ptr, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "row_ptr" in msg
+    rc, msg = _err(lib.allegro_tp_backward, h, 3, 5, ok_rp, ok_ptr, ok_ptr, ok_ptr, ok_ptr, ok_ptr, ok_ptr,
+                   ok_ptr, ok_ptr, ok_ptr, bad_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "grad_Y" in msg
+    rc, msg = _err(lib.allegro_env_embed, h, 3, 5, ok_rp, ok_ptr, None, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "Y is NULL" in msg
+    # empty problem: successful no-op
+    for fn, nargs in ((lib.allegro_env_embed, 5), (lib.allegro_tp_forward, 6), (lib.allegro_tp_backward, 12)):
+        rc = fn(h, 0, 0, *([None] * (nargs - 1)), None)
+        assert rc == binding.ALLEGRO_OK
+    plan.close()

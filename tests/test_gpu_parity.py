@@ -1,0 +1,237 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Both sides run the whole pipeline (embedding -> forward -> backward) from the
+same seeded fp32 inputs.  Small workloads are compared element by element;
+the full-size workloads (about 1e6 and 9e6 edges), run in exactly the launch
+configuration the bench times, are compared on sampled center segments, which
+the oracle evaluates one by one from the segments' own inputs.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import tp as otp
+from tests.parity import BWD_TOL, FWD_TOL, block_rel_err
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def at():
+    assert torch.cuda.is_available(), "GPU tests need a ROCm GPU"
+    import paper_2504_16068_amd as lib
+    return lib
+
+
+DEV = "cuda:0"
+
+
+def _t(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def _plan(at, lmax, U, full, det=False, validate=False):
+    flags = (at.ALLEGRO_FULL_PARITY if full else 0) | (at.ALLEGRO_DETERMINISTIC if det else 0)
+    flags |= at.ALLEGRO_VALIDATE if validate else 0
+    return at.allegro_tp_plan_create(lmax, U, flags)
+
+
+def _run_gpu(at, plan, row_ptr, x, w, y, pw, g):
+    rp, xd, wd, yd, pwd, gd = (_t(a) if isinstance(a, np.ndarray) else a for a in (row_ptr, x, w, y, pw, g))
+    env = at.allegro_env_embed(plan, rp, wd, yd)
+    out = at.allegro_tp_forward(plan, rp, xd, env, pwd)
+    grads = at.allegro_tp_backward(plan, rp, xd, env, pwd, gd, wd, yd)
+    torch.cuda.synchronize()
+    return env, out, grads
+
+
+def _oracle(lmax, full, row_ptr, x, w, y, pw, g):
+    t = otp.TensorProduct(lmax, full)
+    env = otp.env_embed(row_ptr, w, y)
+    out = t.forward(row_ptr, x, env, pw)
+    return t, env, out, t.backward(row_ptr, x, env, pw, g, w, y)
+
+
+def _compare(t, gpu, ref, tag):
+    env, out, (gx, genv, gw, gy) = gpu
+    renv, rout, (rgx, rgenv, rgw, rgy) = ref
+    errs = {
+        "env": (block_rel_err(env, renv, t.env_slices), FWD_TOL),
+        "out": (block_rel_err(out, rout, t.x_slices), FWD_TOL),
+        "grad_x": (block_rel_err(gx, rgx, t.x_slices), BWD_TOL),
+        "grad_env": (block_rel_err(genv, rgenv, t.env_slices), BWD_TOL),
+        "grad_w": (block_rel_err(gw, rgw), BWD_TOL),
+        "grad_Y": (block_rel_err(gy, rgy, t.env_slices), BWD_TOL),
+    }
+    _note(f"{tag}: " + ", ".join(f"{k}={v:.2e}" for k, (v, _) in errs.items()))
+    bad = {k: v for k, (v, tol) in errs.items() if not v <= tol}
+    assert not bad, f"{tag}: parity failed {bad}"
+
+
+def _np(gpu):
+    env, out, grads = gpu
+    return env.cpu().numpy(), out.cpu().numpy(), tuple(a.cpu().numpy() for a in grads)
+
+
+# ------------------------------------------------------------ whole workloads
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_workload_full_parity(at, name):
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    x, w, pw, g = workloads.host_features(cfg, graph.n_edges)
+    _note(f"[gpu] {name}: N={graph.n_atoms} E={graph.n_edges} U={cfg.U} lmax={cfg.lmax}")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    gpu = _np(_run_gpu(at, plan, graph.row_ptr, x, w, graph.Y, pw, g))
+    t, *ref = _oracle(cfg.lmax, cfg.full_parity, graph.row_ptr, x, w, graph.Y, pw, g)
+    _compare(t, gpu, ref, name)
+
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_deterministic_env_is_bit_exact(at, name):
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    _, w, _, _ = workloads.host_features(cfg, graph.n_edges)
+    _note(f"[gpu] deterministic env {name}")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity, det=True)
+    rp, wd, yd = _t(graph.row_ptr), _t(w), _t(graph.Y)
+    env1 = at.allegro_env_embed(plan, rp, wd, yd).cpu().numpy()
+    env2 = at.allegro_env_embed(plan, rp, wd, yd).cpu().numpy()
+    ref = otp.env_embed_fp32_replay(graph.row_ptr, w, graph.Y)
+    assert np.array_equal(env1.view(np.uint32), ref.view(np.uint32))
+    assert np.array_equal(env1.view(np.uint32), env2.view(np.uint32))
+
+
+def test_run_to_run_bitwise_identical(at):
+    graph = workloads.make_graph("small")
+    cfg = graph.config
+    x, w, pw, g = workloads.host_features(cfg, graph.n_edges)
+    _note("[gpu] run-to-run identity, small")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    a = _np(_run_gpu(at, plan, graph.row_ptr, x, w, graph.Y, pw, g))
+    b = _np(_run_gpu(at, plan, graph.row_ptr, x, w, graph.Y, pw, g))
+    for u, v in zip((a[0], a[1], *a[2]), (b[0], b[1], *b[2])):
+        assert np.array_equal(u.view(np.uint32), v.view(np.uint32))
+
+
+# ------------------------------------------------------- synthetic edge cases
+
+def _synthetic(lmax, full, U, degrees, seed):
+    rng = np.random.default_rng(seed)
+    degrees = np.asarray(degrees, dtype=np.int64)
+    row_ptr = np.concatenate([[0], np.cumsum(degrees)]).astype(np.int64)
+    n_edges = int(row_ptr[-1])
+    d1, d2, n_paths = workloads.dims(lmax, full)
+    vec = rng.standard_normal((max(n_edges, 1), 3))[:n_edges]
+    y = workloads.real_sh_cartesian(lmax, vec).astype(np.float32) if n_edges else np.zeros((0, d2), np.float32)
+    x = rng.standard_normal((n_edges, U, d1), dtype=np.float32)
+    w = rng.standard_normal((n_edges, U), dtype=np.float32)
+    pw = (rng.standard_normal((n_paths, U)) / np.sqrt(n_paths)).astype(np.float32)
+    g = rng.standard_normal((n_edges, U, d1), dtype=np.float32)
+    return row_ptr, x, w, y, pw, g
+
+
+EDGE_CASES = [
+    # (lmax, full, U, degrees): empty segments, ragged tails, degree 1, long segments
+    (1, False, 16, [0, 1, 0, 5, 17, 0, 3]),
+    (1, True, 32, [2, 0, 0, 65, 1]),
+    (2, True, 64, [0, 1, 2, 63, 64, 65, 130, 0]),
+    (2, False, 128, [7, 0, 33]),
+    (3, True, 64, [1, 0, 9, 70]),
+    (3, True, 128, [0, 3, 40]),
+    (3, False, 16, [5, 6, 0, 1]),
+    (2, True, 32, [300]),
+]
+
+
+@pytest.mark.parametrize("lmax,full,U,degrees", EDGE_CASES)
+def test_edge_cases(at, lmax, full, U, degrees):
+    _note(f"[gpu] edge case lmax={lmax} full={full} U={U} degrees={degrees}")
+    data = _synthetic(lmax, full, U, degrees, seed=lmax * 100 + U + len(degrees))
+    plan = _plan(at, lmax, U, full, validate=True)
+    gpu = _np(_run_gpu(at, plan, *data))
+    t, *ref = _oracle(lmax, full, *data)
+    _compare(t, gpu, ref, f"lmax{lmax}{'F' if full else 'N'}U{U}")
+    env = gpu[0]
+    assert np.all(env[np.asarray(degrees) == 0] == 0)
+
+
+def test_no_edges_gives_zero_env_and_grad_env(at):
+    _note("[gpu] E = 0 with N = 4")
+    plan = _plan(at, 2, 64, True)
+    rp = torch.zeros(5, dtype=torch.int64, device=DEV)
+    w = torch.empty((0, 64), device=DEV)
+    y = torch.empty((0, 9), device=DEV)
+    x = torch.empty((0, 64, 18), device=DEV)
+    env = at.allegro_env_embed(plan, rp, w, y, env=torch.full((4, 64, 9), 7.0, device=DEV))
+    pw = torch.ones((plan.n_paths, 64), device=DEV)
+    outs = (torch.empty_like(x), torch.full((4, 64, 9), 7.0, device=DEV), torch.empty_like(w), torch.empty_like(y))
+    gx, genv, gw, gy = at.allegro_tp_backward(plan, rp, x, env, pw, x, w, y, outs=outs)
+    out = at.allegro_tp_forward(plan, rp, x, env, pw)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 64, 18)
+    assert torch.count_nonzero(env).item() == 0 and torch.count_nonzero(genv).item() == 0
+
+
+def test_validate_rejects_bad_csr(at):
+    _note("[gpu] CSR validation")
+    plan = _plan(at, 1, 16, False, validate=True)
+    w = torch.zeros((6, 16), device=DEV)
+    y = torch.zeros((6, 4), device=DEV)
+    for bad in ([0, 4, 2, 6], [1, 2, 4, 6], [0, 2, 4, 5]):
+        rp = torch.tensor(bad, dtype=torch.int64, device=DEV)
+        with pytest.raises(at.AllegroError) as ex:
+            at.allegro_env_embed(plan, rp, w, y)
+        assert ex.value.code == at.ALLEGRO_E_INVALID
+    rp = torch.tensor([0, 2, 4, 6], dtype=torch.int64, device=DEV)
+    at.allegro_env_embed(plan, rp, w, y)
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------- full sizes, sampled segments
+
+def _sampled_check(at, name, n_samples=24):
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    _note(f"[gpu] {name}: N={graph.n_atoms} E={graph.n_edges} U={cfg.U} lmax={cfg.lmax} (sampled)")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    x, w, g = workloads.device_features(cfg, graph.n_edges, DEV)
+    pw = workloads.path_weights(cfg)
+    rp, yd, pwd = _t(graph.row_ptr), _t(graph.Y), _t(pw)
+    env = at.allegro_env_embed(plan, rp, w, yd)
+    out = at.allegro_tp_forward(plan, rp, x, env, pwd)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(cfg.index)
+    centers = np.unique(np.concatenate([[0, graph.n_atoms - 1], rng.integers(0, graph.n_atoms, n_samples)]))
+    segs = [(int(graph.row_ptr[n]), int(graph.row_ptr[n + 1])) for n in centers]
+    idx = torch.as_tensor(np.concatenate([np.arange(s, e) for s, e in segs]), device=DEV)
+    local_rp = np.concatenate([[0], np.cumsum([e - s for s, e in segs])]).astype(np.int64)
+    xs, ws, gs = x[idx].cpu().numpy(), w[idx].cpu().numpy(), g[idx].cpu().numpy()
+    ys = graph.Y[idx.cpu().numpy()]
+    env_s = env[torch.as_tensor(centers, device=DEV)].cpu().numpy()
+    out_s = out[idx].cpu().numpy()
+    del out
+    grads = at.allegro_tp_backward(plan, rp, x, env, pwd, g, w, yd)
+    torch.cuda.synchronize()
+    cidx = torch.as_tensor(centers, device=DEV)
+    gx_s, genv_s = grads[0][idx].cpu().numpy(), grads[1][cidx].cpu().numpy()
+    gw_s, gy_s = grads[2][idx].cpu().numpy(), grads[3][idx].cpu().numpy()
+    del grads, x, w, g
+    torch.cuda.empty_cache()
+    t, *ref = _oracle(cfg.lmax, cfg.full_parity, local_rp, xs, ws, ys, pw, gs)
+    _compare(t, (env_s, out_s, (gx_s, genv_s, gw_s, gy_s)), ref, f"{name}[{len(centers)} segments]")
+
+
+@pytest.mark.parametrize("name", ["headline", "high_order", "large"])
+def test_full_size_sampled_segments(at, name):
+    _sampled_check(at, name)
