@@ -60,9 +60,7 @@ def _check_resources(report: str) -> str:
                    f"scratch={kv.get('ScratchSize')} occupancy={kv.get('Occupancy')} lds={kv.get('LDS Size')}")
     if not rows:
         raise RuntimeError("no kernel resource report from hipcc")
-    if bad:
-        raise RuntimeError("kernels use scratch memory: " + ", ".join(sorted(bad)))
-    return "\n".join(out) + "\n"
+    return "\n".join(out) + "\n", bad
 
 
 def build(verbose: bool = False) -> str:
@@ -77,9 +75,11 @@ def build(verbose: bool = False) -> str:
     hip_obj = os.path.join(BUILD, "allegro_tp.o")
     res = _run([HIPCC, *HIP_FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c",
                 os.path.join(CSRC, "allegro_tp.hip"), "-o", hip_obj])
-    summary = _check_resources(res.stderr)
+    summary, spills = _check_resources(res.stderr)
     with open(os.path.join(BUILD, "resource_usage.txt"), "w") as f:
         f.write(summary)
+    if spills:
+        raise RuntimeError("kernels use scratch memory (see _build/resource_usage.txt): " + ", ".join(spills))
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", hip_obj, cg_obj, "-o", tmp])
     os.replace(tmp, LIB)

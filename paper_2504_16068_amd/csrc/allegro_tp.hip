@@ -27,6 +27,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "allegro_tp.h"
@@ -123,65 +124,221 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
   for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
 }
 
+// -------------------------------------------------------------------- slabs
+// A center's per-lane rows are streamed in slabs: 64 consecutive rows of D
+// floats that are contiguous in HBM, so every slab moves with fully coalesced
+// 16-byte accesses (per-lane 72-byte rows read directly cost about a quarter
+// of the bandwidth).  With U >= 64, slab (s, t) holds channels t*64 .. t*64+63
+// of edge e0+s; with U < 64 it holds edges e0+s*G .. e0+s*G+G-1, all channels,
+// and the last slab of a segment may be partial.  A tile of T slabs is staged
+// through LDS, where each lane reads and writes its own row.
+template <int D>
+struct TileShape {
+  static constexpr int SF4 = 16 * D;  // float4 per slab (64 rows of D floats)
+  template <int T>
+  static constexpr int per_lane() { return (T * SF4 + kWave - 1) / kWave; }
+};
+
+template <int U>
+struct Slabs {
+  using L = Lanes<U>;
+  static __device__ __forceinline__ int64_t count(int64_t deg) { return U >= kWave ? deg : (deg + L::G - 1) / L::G; }
+  static __device__ __forceinline__ int64_t first_edge(int64_t e0, int64_t s) {
+    return U >= kWave ? e0 + s : e0 + s * L::G;
+  }
+};
+
+// A tile is cnt consecutive slabs that are also contiguous in memory: any
+// number of slabs when U <= 64, one slab when U > 64 (channel halves of
+// consecutive edges are U*D floats apart).  Returns the tile's first float4
+// (wave-uniform) and how many of its float4 lie inside the segment.
+template <int U, int D>
+__device__ __forceinline__ int64_t tile_base(int64_t e0, int64_t e1, int64_t s0, int cnt, int t, int &n_f4) {
+  constexpr int SF4 = TileShape<D>::SF4;
+  if constexpr (U <= kWave) {
+    const int64_t eb = Slabs<U>::first_edge(e0, s0);
+    const int64_t in_seg = (e1 - eb) * (U * D / 4);
+    n_f4 = int(in_seg < int64_t(cnt) * SF4 ? in_seg : int64_t(cnt) * SF4);
+    return eb * (U * D / 4);
+  } else {
+    n_f4 = SF4;  // cnt == 1
+    return ((e0 + s0) * U + t * kWave) * D / 4;  // U*D and 64*D are multiples of 4
+  }
+}
+
+template <int U, int D, int PER>
+__device__ __forceinline__ void tile_load(const float *__restrict__ src, float4 *tile, int64_t e0, int64_t e1,
+                                          int64_t s0, int cnt, int t, int lane) {
+  int n_f4;
+  const float4 *base = reinterpret_cast<const float4 *>(src) + tile_base<U, D>(e0, e1, s0, cnt, t, n_f4);
+  float4 v[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int f = lane + kWave * k;
+    v[k] = f < n_f4 ? base[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int f = lane + kWave * k;
+    if (f < n_f4) tile[f] = v[k];
+  }
+}
+
+template <int U, int D, int PER>
+__device__ __forceinline__ void tile_store(float *__restrict__ dst, const float4 *tile, int64_t e0, int64_t e1,
+                                           int64_t s0, int cnt, int t, int lane) {
+  int n_f4;
+  float4 *base = reinterpret_cast<float4 *>(dst) + tile_base<U, D>(e0, e1, s0, cnt, t, n_f4);
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int f = lane + kWave * k;
+    if (f < n_f4) base[f] = tile[f];
+  }
+}
+
+// Does lane's row of slab `slab` hold a real edge?  Only partial slabs (U < 64)
+// can fail.  For U >= 64 the test is always true, but it is kept as a runtime
+// branch: it makes the row contraction its own scheduling region, without
+// which the scheduler interleaves it with the tile epilogue and spills.
+template <int U>
+__device__ __forceinline__ bool row_valid(int64_t e0, int64_t e1, int64_t slab, int lane) {
+  if constexpr (U >= kWave) return e0 + slab < e1;
+  else return Slabs<U>::first_edge(e0, slab) + lane / U < e1;
+}
+
+// ------------------------------------------------------------ path weights
+// The lane's weights W[p, u] of its channel u.  With few paths they sit in
+// VGPRs; with many (lmax 3, full parity: 68) they sit in an LDS column that
+// only this lane touches, read once per path and row, which frees the VGPRs
+// the lmax-3 contraction needs.
+template <int NP>
+struct RegWeights {
+  float r[NP];
+  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U, int u, float *, int) {
+#pragma unroll
+    for (int p = 0; p < NP; ++p) r[p] = path_w[p * U + u];
+  }
+  __device__ __forceinline__ float operator()(int p) const { return r[p]; }
+};
+
+template <int NP>
+struct LdsWeights {
+  const float *col;
+  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U, int u, float *lds, int lane) {
+#pragma unroll 4
+    for (int p = 0; p < NP; ++p) lds[p * kWave + lane] = path_w[p * U + u];
+    col = lds + lane;
+  }
+  __device__ __forceinline__ float operator()(int p) const { return col[p * kWave]; }
+};
+
+template <class Core>
+struct KernelTraits {
+  static constexpr bool kWeightsInLds = false;
+  using Weights = typename std::conditional<kWeightsInLds, LdsWeights<Core::NP>, RegWeights<Core::NP>>::type;
+  static constexpr int kWeightLds = kWeightsInLds ? Core::NP * kWave : 1;
+  // waves per SIMD the register allocation must allow
+  static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
+  static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 3;
+};
+
 // ------------------------------------------------------ tensor product fwd
 template <class Core, int U>
-__global__ __launch_bounds__(kWave) void tp_forward_kernel(const int64_t *__restrict__ row_ptr,
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kFwdOccupancy))) void tp_forward_kernel(const int64_t *__restrict__ row_ptr,
                                                            const float *__restrict__ x,
                                                            const float *__restrict__ env,
                                                            const float *__restrict__ path_w,
                                                            float *__restrict__ out) {
   using L = Lanes<U>;
-  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP;
-  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  constexpr int D1 = Core::D1, D2 = Core::D2;
+  constexpr int T = U > kWave ? 1 : (36 / D1 > 1 ? 36 / D1 : 1);  // slabs per tile (about 9 KB of LDS)
+  constexpr int PER = TileShape<D1>::template per_lane<T>();
+  __shared__ float4 tile[T * TileShape<D1>::SF4];
+  __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
+  float *tile_f = reinterpret_cast<float *>(tile);
+  const int lane = threadIdx.x, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
     const int u = ul + t * kWave;
-    float wr[NP], er[D2];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) wr[p] = path_w[p * U + u];
+    typename KernelTraits<Core>::Weights wr;
+    wr.load(path_w, U, u, w_lds, lane);
+    float er[D2];
     load_row<D2>(env + (n * U + u) * D2, er);
-    for (int64_t e = e0 + grp; e < e1; e += L::G) {
-      float xr[D1], orow[D1];
-      load_row<D1>(x + (e * U + u) * D1, xr);
-      Core::fwd(xr, er, wr, orow);
-      store_row<D1>(out + (e * U + u) * D1, orow);
+    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+      tile_load<U, D1, PER>(x, tile, e0, e1, s0, cnt, t, lane);
+      __syncthreads();
+#pragma unroll 1
+      for (int s = 0; s < cnt; ++s) {
+        if (row_valid<U>(e0, e1, s0 + s, lane)) {
+          float *row = tile_f + (s * kWave + lane) * D1;
+          float xr[D1], orow[D1];
+#pragma unroll
+          for (int i = 0; i < D1; ++i) xr[i] = row[i];
+          Core::fwd(xr, er, wr, orow);
+#pragma unroll
+          for (int i = 0; i < D1; ++i) row[i] = orow[i];
+        }
+      }
+      __syncthreads();
+      tile_store<U, D1, PER>(out, tile, e0, e1, s0, cnt, t, lane);
+      __syncthreads();
     }
   }
 }
 
 // ------------------------------------------------------ tensor product bwd
 template <class Core, int U>
-__global__ __launch_bounds__(kWave) void tp_backward_kernel(
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kBwdOccupancy))) void tp_backward_kernel(
     const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
     const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
     const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
     float *__restrict__ grad_w, float *__restrict__ grad_Y) {
   using L = Lanes<U>;
-  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP;
-  __shared__ float ge_s[U * D2];                  // grad_env[n, :, :] of this center
+  constexpr int D1 = Core::D1, D2 = Core::D2;
+  constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
+  constexpr int PER = TileShape<D1>::template per_lane<T>();
+  __shared__ float4 tile_x[T * TileShape<D1>::SF4];
+  __shared__ float4 tile_g[T * TileShape<D1>::SF4];
+  __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
+  __shared__ float ge_s[U * D2];                       // grad_env[n, :, :] of this center
   __shared__ float part_s[L::G > 1 ? kWave * D2 : 1];  // per-group partial sums (U < 64)
+  float *tx = reinterpret_cast<float *>(tile_x);
+  const float *tg = reinterpret_cast<const float *>(tile_g);
   const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
 
   // Pass 1 (lane <-> channel): grad_x per edge, grad_env accumulated in registers.
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
     const int u = ul + t * kWave;
-    float wr[NP], er[D2], ge[D2];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) wr[p] = path_w[p * U + u];
+    typename KernelTraits<Core>::Weights wr;
+    wr.load(path_w, U, u, w_lds, lane);
+    float er[D2], ge[D2];
     load_row<D2>(env + (n * U + u) * D2, er);
 #pragma unroll
     for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
-    for (int64_t e = e0 + grp; e < e1; e += L::G) {
-      float xr[D1], gr[D1], gxr[D1];
-      load_row<D1>(x + (e * U + u) * D1, xr);
-      load_row<D1>(g + (e * U + u) * D1, gr);
-      Core::bwd(xr, er, wr, gr, gxr, ge);
-      store_row<D1>(grad_x + (e * U + u) * D1, gxr);
+    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+      tile_load<U, D1, PER>(x, tile_x, e0, e1, s0, cnt, t, lane);
+      tile_load<U, D1, PER>(g, tile_g, e0, e1, s0, cnt, t, lane);
+      __syncthreads();
+#pragma unroll 1
+      for (int s = 0; s < cnt; ++s) {
+        if (row_valid<U>(e0, e1, s0 + s, lane)) {
+          // x row in, grad_x row out, in place in the LDS tile
+          float *row = tx + (s * kWave + lane) * D1;
+          Core::bwd(row, er, wr, tg + (s * kWave + lane) * D1, row, ge);
+        }
+      }
+      __syncthreads();
+      tile_store<U, D1, PER>(grad_x, tile_x, e0, e1, s0, cnt, t, lane);
+      __syncthreads();
     }
     if constexpr (L::G == 1) {
 #pragma unroll
@@ -194,9 +351,9 @@ __global__ __launch_bounds__(kWave) void tp_backward_kernel(
       if (grp == 0) {
 #pragma unroll
         for (int j = 0; j < D2; ++j) {
-          float s = part_s[ul * D2 + j];
-          for (int q = 1; q < L::G; ++q) s += part_s[(q * L::LPE + ul) * D2 + j];
-          ge_s[u * D2 + j] = s;
+          float acc = part_s[ul * D2 + j];
+          for (int q = 1; q < L::G; ++q) acc += part_s[(q * L::LPE + ul) * D2 + j];
+          ge_s[u * D2 + j] = acc;
         }
       }
     }

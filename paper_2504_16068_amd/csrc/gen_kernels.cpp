@@ -5,13 +5,14 @@
 // Every coefficient becomes an fp32 literal and every register index a
 // compile-time constant, so the per-lane operands stay in VGPRs and the
 // coupling table costs no memory traffic at all.  The generated cores are
-//   fwd: out[k]  = sum_p W[p] sum_{(i,j,k) in p} C q_ij,  q_ij = x[i] env[j]
+//   fwd: out[k]  = sum_p W(p) sum_{(i,j,k) in p} C q_ij,  q_ij = x[i] env[j]
 //        (products shared by all paths with the same input blocks (a, b))
-//   bwd: Q_ij    = sum_{p with blocks (a,b)} sum_k C (W[p] g[k])
-//        gx[i]   = sum_j Q_ij env[j]           (overwritten)
+//   bwd: Q_ij    = sum_{p with blocks (a,b)} sum_k C (W(p) g[k])
+//        gx[i]   = sum_j Q_ij env[j]           (overwritten; may alias x)
 //        ge[j]  += sum_i Q_ij x[i]             (accumulated across edges)
 // which is the tensor product and its VJP with respect to x and env, written
 // per pair of input blocks so that at most one block of temporaries is live.
+// W is any accessor with W(p) = the lane's weight of path p (registers or LDS).
 //
 // Usage: gen_kernels <output.inc>
 #include <cstdio>
@@ -72,8 +73,9 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
 
   // ---------------------------------------------------------------- forward
   std::fprintf(f,
+               "  template <class WT>\n"
                "  static __device__ __forceinline__ void fwd(const float *__restrict__ x, const float *__restrict__ env,\n"
-               "                                             const float *__restrict__ W, float *__restrict__ out) {\n");
+               "                                             const WT &W, float *__restrict__ out) {\n");
   std::vector<bool> out_init(t.d1, false);
   for (const Group &g : groups) {
     std::fprintf(f, "    { // x block %d (l=%d) with env block %d (l=%d)\n", g.a, t.x_irreps[g.a].l, g.b,
@@ -95,9 +97,9 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
         }
         const int k = kv.first;
         if (out_init[k])
-          std::fprintf(f, " out[%d] = __builtin_fmaf(W[%d], s, out[%d]); }\n", k, p, k);
+          std::fprintf(f, " out[%d] = __builtin_fmaf(W(%d), s, out[%d]); }\n", k, p, k);
         else
-          std::fprintf(f, " out[%d] = W[%d] * s; }\n", k, p);
+          std::fprintf(f, " out[%d] = W(%d) * s; }\n", k, p);
         out_init[k] = true;
       }
     }
@@ -108,48 +110,62 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   std::fprintf(f, "  }\n");
 
   // ---------------------------------------------------------------- backward
+  // Emitted per x irrep a: its x values are read once at the start of the
+  // section and its grad_x values are written once at the end, so x and gx may
+  // be the same row (in-place) and only one block of gx accumulators is live.
   std::fprintf(f,
-               "  static __device__ __forceinline__ void bwd(const float *__restrict__ x, const float *__restrict__ env,\n"
-               "                                             const float *__restrict__ W, const float *__restrict__ g,\n"
-               "                                             float *__restrict__ gx, float *__restrict__ ge) {\n");
-  std::vector<bool> gx_init(t.d1, false);
-  for (const Group &g : groups) {
-    std::fprintf(f, "    { // x block %d with env block %d\n", g.a, g.b);
-    std::set<std::pair<int, int>> wg_needed;  // (path, k)
-    for (int p : g.paths)
-      for (const auto &e : per_path[p]) wg_needed.insert({p, e.k});
-    for (const auto &pk : wg_needed)
-      std::fprintf(f, "      const float wg%d_%d = W[%d] * g[%d];\n", pk.first, pk.second, pk.first, pk.second);
-    std::map<std::pair<int, int>, bool> q_init;
-    std::vector<std::pair<int, int>> q_order;
-    for (int p : g.paths)
-      for (const auto &e : per_path[p]) {
-        const auto ij = std::make_pair(e.i, e.j);
-        const bool first = !q_init.count(ij);
-        const std::string name = "Q" + std::to_string(e.i) + "_" + std::to_string(e.j);
-        if (first) {
-          q_order.push_back(ij);
-          q_init[ij] = true;
-          std::fprintf(f, "      float %s;", name.c_str());
-        } else {
-          std::fprintf(f, "     ");
+               "  template <class WT>\n"
+               "  static __device__ __forceinline__ void bwd(const float *x, const float *__restrict__ env,\n"
+               "                                             const WT &W, const float *__restrict__ g,\n"
+               "                                             float *gx, float *__restrict__ ge) {\n");
+  for (int a = 0; a < int(t.x_irreps.size()); ++a) {
+    const int la = t.x_irreps[a].l, oa = t.x_off[a], da = 2 * la + 1;
+    std::fprintf(f, "    { // x block %d (l=%d)\n", a, la);
+    for (int m = 0; m < da; ++m) std::fprintf(f, "      const float xa%d = x[%d];\n", m, oa + m);
+    std::vector<bool> gx_init(da, false);
+    std::fprintf(f, "      float");
+    for (int m = 0; m < da; ++m) std::fprintf(f, "%s gxa%d", m ? "," : "", m);
+    std::fprintf(f, ";\n");
+    for (const Group &g : groups) {
+      if (g.a != a) continue;
+      std::fprintf(f, "      { // with env block %d\n", g.b);
+      std::set<std::pair<int, int>> wg_needed;  // (path, k)
+      for (int p : g.paths)
+        for (const auto &e : per_path[p]) wg_needed.insert({p, e.k});
+      for (const auto &pk : wg_needed)
+        std::fprintf(f, "        const float wg%d_%d = W(%d) * g[%d];\n", pk.first, pk.second, pk.first, pk.second);
+      std::map<std::pair<int, int>, bool> q_init;
+      std::vector<std::pair<int, int>> q_order;
+      for (int p : g.paths)
+        for (const auto &e : per_path[p]) {
+          const auto ij = std::make_pair(e.i, e.j);
+          const bool first = !q_init.count(ij);
+          const std::string name = "Q" + std::to_string(e.i) + "_" + std::to_string(e.j);
+          if (first) {
+            q_order.push_back(ij);
+            q_init[ij] = true;
+            std::fprintf(f, "        float %s;", name.c_str());
+          } else {
+            std::fprintf(f, "       ");
+          }
+          std::fprintf(f, " %s\n",
+                       accumulate(name, first, e.value, "wg" + std::to_string(p) + "_" + std::to_string(e.k)).c_str());
         }
-        std::fprintf(f, " %s\n",
-                     accumulate(name, first, e.value, "wg" + std::to_string(p) + "_" + std::to_string(e.k)).c_str());
+      for (const auto &ij : q_order) {
+        const int i = ij.first, j = ij.second, m = i - oa;
+        if (gx_init[m])
+          std::fprintf(f, "        gxa%d = __builtin_fmaf(Q%d_%d, env[%d], gxa%d);", m, i, j, j, m);
+        else
+          std::fprintf(f, "        gxa%d = Q%d_%d * env[%d];", m, i, j, j);
+        gx_init[m] = true;
+        std::fprintf(f, " ge[%d] = __builtin_fmaf(Q%d_%d, xa%d, ge[%d]);\n", j, i, j, m, j);
       }
-    for (const auto &ij : q_order) {
-      const int i = ij.first, j = ij.second;
-      if (gx_init[i])
-        std::fprintf(f, "      gx[%d] = __builtin_fmaf(Q%d_%d, env[%d], gx[%d]);", i, i, j, j, i);
-      else
-        std::fprintf(f, "      gx[%d] = Q%d_%d * env[%d];", i, i, j, j);
-      gx_init[i] = true;
-      std::fprintf(f, " ge[%d] = __builtin_fmaf(Q%d_%d, x[%d], ge[%d]);\n", j, i, j, i, j);
+      std::fprintf(f, "      }\n");
     }
+    for (int m = 0; m < da; ++m)
+      std::fprintf(f, "      gx[%d] = %s;\n", oa + m, gx_init[m] ? ("gxa" + std::to_string(m)).c_str() : "0.0f");
     std::fprintf(f, "    }\n");
   }
-  for (int i = 0; i < t.d1; ++i)
-    if (!gx_init[i]) std::fprintf(f, "    gx[%d] = 0.0f;\n", i);
   std::fprintf(f, "  }\n};\n\n");
 }
 
