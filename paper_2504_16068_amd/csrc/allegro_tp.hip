@@ -84,6 +84,20 @@ __device__ __forceinline__ void store_row(float *__restrict__ p, const float (&r
   }
 }
 
+// Streaming 16-byte accesses with the non-temporal hint: x, g, out and grad_x
+// are touched once per kernel, so they should not displace other lines in L2.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 load_stream(const float4 *p) {
+  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ void store_stream(float4 v, float4 *p) {
+  const f32x4 w = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(w, reinterpret_cast<f32x4 *>(p));
+}
+
 // acc + fl(a * b) with two separate roundings (no contraction to FMA).
 __device__ __forceinline__ float add_rounded_product(float acc, float a, float b) {
 #pragma clang fp contract(off)
@@ -93,14 +107,29 @@ __device__ __forceinline__ float add_rounded_product(float acc, float a, float b
 
 // ------------------------------------------------------------ env embedding
 // env[n,u,j] = sum_{e in seg(n)} w[e,u] Y[e,j].  Lane groups take different
-// centers (U < 64) so every env value is one lane's ascending-e sum.
+// centers (U < 64) so every env value is one lane's ascending-e sum.  The
+// loads of B edges are issued together and then accumulated in edge order,
+// so the summation order (and the deterministic mode's bits) does not change.
+template <int U, int D2, bool DET>
+__device__ __forceinline__ void env_accumulate(float (&acc)[Lanes<U>::CPL][D2], const float (&wv)[Lanes<U>::CPL],
+                                               const float (&y)[D2]) {
+#pragma unroll
+  for (int t = 0; t < Lanes<U>::CPL; ++t)
+#pragma unroll
+    for (int j = 0; j < D2; ++j)
+      acc[t][j] = DET ? add_rounded_product(acc[t][j], wv[t], y[j]) : __builtin_fmaf(wv[t], y[j], acc[t][j]);
+}
+
 template <int U, int D2, bool DET>
 __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64_t *__restrict__ row_ptr,
                                                           const float *__restrict__ w,
                                                           const float *__restrict__ Y, float *__restrict__ env) {
   using L = Lanes<U>;
+  constexpr int B = D2 <= 9 ? 8 : 4;  // edges whose loads are in flight together
   const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
-  const int64_t n = int64_t(blockIdx.x) * L::G + grp;
+  // with one group per wave the center (hence e and every Y address) is
+  // wave-uniform, so Y rows come through scalar loads
+  const int64_t n = L::G == 1 ? int64_t(blockIdx.x) : int64_t(blockIdx.x) * L::G + grp;
   if (n >= N) return;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
   float acc[L::CPL][D2];
@@ -108,17 +137,26 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
   for (int t = 0; t < L::CPL; ++t)
 #pragma unroll
     for (int j = 0; j < D2; ++j) acc[t][j] = 0.0f;
-  for (int64_t e = e0; e < e1; ++e) {
-    float y[D2];
+  int64_t e = e0;
+  for (; e + B <= e1; e += B) {
+    float wv[B][L::CPL], y[B][D2];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+#pragma unroll
+      for (int j = 0; j < D2; ++j) y[b][j] = Y[(e + b) * D2 + j];
+#pragma unroll
+      for (int t = 0; t < L::CPL; ++t) wv[b][t] = w[(e + b) * U + ul + t * kWave];
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) env_accumulate<U, D2, DET>(acc, wv[b], y[b]);
+  }
+  for (; e < e1; ++e) {
+    float wv[L::CPL], y[D2];
 #pragma unroll
     for (int j = 0; j < D2; ++j) y[j] = Y[e * D2 + j];
 #pragma unroll
-    for (int t = 0; t < L::CPL; ++t) {
-      const float wv = w[e * U + ul + t * kWave];
-#pragma unroll
-      for (int j = 0; j < D2; ++j)
-        acc[t][j] = DET ? add_rounded_product(acc[t][j], wv, y[j]) : __builtin_fmaf(wv, y[j], acc[t][j]);
-    }
+    for (int t = 0; t < L::CPL; ++t) wv[t] = w[e * U + ul + t * kWave];
+    env_accumulate<U, D2, DET>(acc, wv, y);
   }
 #pragma unroll
   for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
@@ -175,7 +213,7 @@ __device__ __forceinline__ void tile_load(const float *__restrict__ src, float4 
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int f = lane + kWave * k;
-    v[k] = f < n_f4 ? base[f] : make_float4(0.f, 0.f, 0.f, 0.f);
+    v[k] = f < n_f4 ? load_stream(base + f) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -192,7 +230,7 @@ __device__ __forceinline__ void tile_store(float *__restrict__ dst, const float4
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int f = lane + kWave * k;
-    if (f < n_f4) base[f] = tile[f];
+    if (f < n_f4) store_stream(tile[f], base + f);
   }
 }
 
@@ -301,11 +339,12 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   constexpr int D1 = Core::D1, D2 = Core::D2;
   constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
   constexpr int PER = TileShape<D1>::template per_lane<T>();
-  __shared__ float4 tile_x[T * TileShape<D1>::SF4];
-  __shared__ float4 tile_g[T * TileShape<D1>::SF4];
+  constexpr int TILE_F4 = T * TileShape<D1>::SF4;
+  __shared__ float4 tiles[2 * TILE_F4];                // x and g tiles (pass 1), w rows (pass 2)
   __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
   __shared__ float ge_s[U * D2];                       // grad_env[n, :, :] of this center
   __shared__ float part_s[L::G > 1 ? kWave * D2 : 1];  // per-group partial sums (U < 64)
+  float4 *tile_x = tiles, *tile_g = tiles + TILE_F4;
   float *tx = reinterpret_cast<float *>(tile_x);
   const float *tg = reinterpret_cast<const float *>(tile_g);
   const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
@@ -361,30 +400,58 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   __syncthreads();
   for (int i = lane; i < U * D2; i += kWave) grad_env[n * U * D2 + i] = ge_s[i];
 
-  // Pass 2 (lane <-> edge): grad_w[e,u] = sum_j ge[u,j] Y[e,j], grad_Y[e,j] = sum_u ge[u,j] w[e,u].
-  for (int64_t e = e0 + lane; e < e1; e += kWave) {
-    float y[D2], gy[D2];
-    load_row<D2>(Y + e * D2, y);
+  // Pass 2: the embedding's VJP through grad_env, in batches of EB edges whose w and
+  // Y rows are first staged into the (now free) tile memory with one round of
+  // coalesced loads:
+  //   grad_w[e,u] = sum_j grad_env[n,u,j] Y[e,j]   lane <-> channel (coalesced stores)
+  //   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> edge; grad_env from LDS
+  //                                                as wave-uniform broadcasts
+  // w rows are padded to U+1 floats so the per-lane row reads hit distinct banks.
+  constexpr int WROW = U + 1;
+  constexpr int TILE_FLOATS = 2 * TILE_F4 * 4;
+  constexpr int EB = TILE_FLOATS / (WROW + D2) < kWave ? TILE_FLOATS / (WROW + D2) : kWave;
+  static_assert(EB >= 1, "tile memory too small for one w row");
+  float *wl = reinterpret_cast<float *>(tiles);
+  float *yl = wl + EB * WROW;
+  const float4 *w4 = reinterpret_cast<const float4 *>(w);
+  float gel[L::CPL][D2];
 #pragma unroll
-    for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
-#pragma unroll 1
-    for (int u0 = 0; u0 < U; u0 += 4) {
-      float wv[4], gw[4];
-      load_row<4>(w + e * U + u0, wv);
+  for (int t = 0; t < L::CPL; ++t)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
+    for (int j = 0; j < D2; ++j) gel[t][j] = ge_s[(ul + t * kWave) * D2 + j];
+  for (int64_t eb = e0; eb < e1; eb += EB) {
+    const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
+    __syncthreads();  // the previous batch (or pass 1) is done with the tile memory
+    for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
+      const float4 v = w4[eb * (U / 4) + i4];
+      const int r = (4 * i4) / U, c = (4 * i4) % U;
+      float *dst = wl + r * WROW + c;
+      dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+    }
+    for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
+    __syncthreads();
+    for (int k = grp; k < cnt; k += L::G) {
+#pragma unroll
+      for (int t = 0; t < L::CPL; ++t) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = 0; j < D2; ++j) {
-          const float gej = ge_s[(u0 + c) * D2 + j];
-          acc = __builtin_fmaf(gej, y[j], acc);
-          gy[j] = __builtin_fmaf(gej, wv[c], gy[j]);
-        }
-        gw[c] = acc;
+        for (int j = 0; j < D2; ++j) acc = __builtin_fmaf(gel[t][j], yl[k * D2 + j], acc);
+        grad_w[(eb + k) * U + ul + t * kWave] = acc;
       }
-      store_row<4>(grad_w + e * U + u0, gw);
     }
-    store_row<D2>(grad_Y + e * D2, gy);
+    if (lane < cnt) {
+      const float *wrow = wl + lane * WROW;
+      float gy[D2];
+#pragma unroll
+      for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
+#pragma unroll 4
+      for (int u = 0; u < U; ++u) {
+        const float wv = wrow[u];
+#pragma unroll
+        for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(ge_s[u * D2 + j], wv, gy[j]);
+      }
+      store_row<D2>(grad_Y + (eb + lane) * D2, gy);
+    }
   }
 }
 

@@ -164,6 +164,9 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
     }
     for (int m = 0; m < da; ++m)
       std::fprintf(f, "      gx[%d] = %s;\n", oa + m, gx_init[m] ? ("gxa" + std::to_string(m)).c_str() : "0.0f");
+    // keep the machine scheduler from merging sections (it would hoist every
+    // section's loads and spill); one section's temporaries are live at a time
+    std::fprintf(f, "      __builtin_amdgcn_sched_barrier(0);\n");
     std::fprintf(f, "    }\n");
   }
   std::fprintf(f, "  }\n};\n\n");
