@@ -16,6 +16,7 @@ with HIP events on the stream the library launches on.  cpu_baseline times
 the fp64 oracle (single thread) on a prefix of whole center segments.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+       python bench.py --pmc-summary FETCH_CSV WRITE_CSV   (after two rocprofv3 --pmc runs)
 """
 
 from __future__ import annotations
@@ -79,6 +80,45 @@ def measured_traffic(workload: str):
     return rec.get("traffic_bytes_per_launch")
 
 
+def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
+    """Calibrated HBM traffic of tp_backward from two rocprofv3 --pmc runs of this script.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same
+    counter reads for the 4 GiB device copy that copy_bandwidth() performs
+    (__amd_rocclr_copyBuffer), so that request-size conventions of the counters
+    cancel out.  Writes the record bench.py reads as roofline.traffic.
+    """
+    import csv
+
+    def read(path):
+        with open(path) as f:
+            return list(csv.DictReader(f))
+
+    copy_kib = (4 << 30) / 1024
+
+    def per_launch(rows, kernel):
+        vals = [float(r["Counter_Value"]) for r in rows if kernel in r["Kernel_Name"]]
+        return sum(vals) / len(vals), len(vals)
+
+    fr, wr = read(fetch_csv), read(write_csv)
+    f_copy = max(float(r["Counter_Value"]) for r in fr if "copyBuffer" in r["Kernel_Name"])
+    w_copy = max(float(r["Counter_Value"]) for r in wr if "copyBuffer" in r["Kernel_Name"])
+    f_b, n_f = per_launch(fr, "tp_backward_kernel")
+    w_b, _ = per_launch(wr, "tp_backward_kernel")
+    graph = workloads.make_graph(workload)
+    algo = algorithmic_bytes(graph.config, graph.n_atoms, graph.n_edges)["tp_backward"]
+    traffic = (f_b * copy_kib / f_copy + w_b * copy_kib / w_copy) * 1024
+    rec = {"workload": workload, "kernel": "tp_backward", "kernel_source_digest": kernel_source_digest(),
+           "fetch_kib_per_dispatch": f_b, "write_kib_per_dispatch": w_b, "dispatches": n_f,
+           "copy_calibration": {"copy_bytes": 4 << 30, "fetch_kib": f_copy, "write_kib": w_copy,
+                                "fetch_scale": copy_kib / f_copy, "write_scale": copy_kib / w_copy},
+           "traffic_bytes_per_launch": traffic, "algorithmic_bytes_per_launch": algo,
+           "traffic_over_algorithmic": traffic / algo}
+    with open(out_path, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def copy_bandwidth(torch, dev, n_bytes=4 << 30, reps=10):
     src = torch.empty(n_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
     dst = torch.empty_like(src)
@@ -126,7 +166,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="headline", choices=sorted(workloads.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the calibrated tp_backward traffic record from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, args.workload, PROFILE_TRAFFIC)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the tensor product shards by center ranges with no "
               "communication inside the path, and multi-GPU runs are not part of this build.", file=sys.stderr)
