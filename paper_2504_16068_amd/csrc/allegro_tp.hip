@@ -340,13 +340,23 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
   constexpr int PER = TileShape<D1>::template per_lane<T>();
   constexpr int TILE_F4 = T * TileShape<D1>::SF4;
-  __shared__ float4 tiles[2 * TILE_F4];                // x and g tiles (pass 1), w rows (pass 2)
+  // One LDS buffer serves both passes: the x and g tiles in pass 1; in pass 2
+  // grad_env[n] of all channels followed by staged w and Y rows (at least
+  // kMinBatch edges) or, with several lane groups, their partial sums.
+  constexpr int WROW = U + 1;  // padded w row: per-lane row reads hit distinct banks
+  constexpr int kMinBatch = 8;
+  constexpr int P1_FLOATS = 2 * TILE_F4 * 4;
+  constexpr int PART_FLOATS = L::G > 1 ? kWave * D2 : 0;
+  constexpr int ROWS_FLOATS = kMinBatch * (WROW + D2);
+  constexpr int P2_FLOATS = U * D2 + (PART_FLOATS > ROWS_FLOATS ? PART_FLOATS : ROWS_FLOATS);
+  constexpr int SMEM_FLOATS = P1_FLOATS > P2_FLOATS ? P1_FLOATS : P2_FLOATS;
+  __shared__ float4 smem[(SMEM_FLOATS + 3) / 4];
   __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
-  __shared__ float ge_s[U * D2];                       // grad_env[n, :, :] of this center
-  __shared__ float part_s[L::G > 1 ? kWave * D2 : 1];  // per-group partial sums (U < 64)
-  float4 *tile_x = tiles, *tile_g = tiles + TILE_F4;
+  float4 *tile_x = smem, *tile_g = smem + TILE_F4;
   float *tx = reinterpret_cast<float *>(tile_x);
   const float *tg = reinterpret_cast<const float *>(tile_g);
+  float *ge_l = reinterpret_cast<float *>(smem);  // pass 2: grad_env[n, :, :]
+  float *rest = ge_l + U * D2;                    // pass 2: group partials, then w / Y rows
   const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
@@ -379,26 +389,39 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
       tile_store<U, D1, PER>(grad_x, tile_x, e0, e1, s0, cnt, t, lane);
       __syncthreads();
     }
+    // grad_env of this channel half goes straight to its output (the tile loop's
+    // last barrier has passed, so the LDS buffer is free for the group partials)
     if constexpr (L::G == 1) {
-#pragma unroll
-      for (int j = 0; j < D2; ++j) ge_s[u * D2 + j] = ge[j];
+      store_row<D2>(grad_env + (n * U + u) * D2, ge);
     } else {
       // combine the lane groups in a fixed order
 #pragma unroll
-      for (int j = 0; j < D2; ++j) part_s[lane * D2 + j] = ge[j];
+      for (int j = 0; j < D2; ++j) rest[lane * D2 + j] = ge[j];
       __syncthreads();
       if (grp == 0) {
+        float acc[D2];
 #pragma unroll
         for (int j = 0; j < D2; ++j) {
-          float acc = part_s[ul * D2 + j];
-          for (int q = 1; q < L::G; ++q) acc += part_s[(q * L::LPE + ul) * D2 + j];
-          ge_s[u * D2 + j] = acc;
+          acc[j] = rest[ul * D2 + j];
+          for (int q = 1; q < L::G; ++q) acc[j] += rest[(q * L::LPE + ul) * D2 + j];
         }
+        store_row<D2>(grad_env + (n * U + u) * D2, acc);
       }
     }
   }
   __syncthreads();
-  for (int i = lane; i < U * D2; i += kWave) grad_env[n * U * D2 + i] = ge_s[i];
+  // Stage grad_env[n] in LDS for pass 2.  Every lane copies back only values it
+  // stored itself, so program order alone makes them visible to it.
+  if (grp == 0) {
+#pragma unroll
+    for (int t = 0; t < L::CPL; ++t) {
+      float v[D2];
+      load_row<D2>(grad_env + (n * U + ul + t * kWave) * D2, v);
+#pragma unroll
+      for (int j = 0; j < D2; ++j) ge_l[(ul + t * kWave) * D2 + j] = v[j];
+    }
+  }
+  __syncthreads();
 
   // Pass 2: the embedding's VJP through grad_env, in batches of EB edges whose w and
   // Y rows are first staged into the (now free) tile memory with one round of
@@ -407,21 +430,20 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   //   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> edge; grad_env from LDS
   //                                                as wave-uniform broadcasts
   // w rows are padded to U+1 floats so the per-lane row reads hit distinct banks.
-  constexpr int WROW = U + 1;
-  constexpr int TILE_FLOATS = 2 * TILE_F4 * 4;
-  constexpr int EB = TILE_FLOATS / (WROW + D2) < kWave ? TILE_FLOATS / (WROW + D2) : kWave;
-  static_assert(EB >= 1, "tile memory too small for one w row");
-  float *wl = reinterpret_cast<float *>(tiles);
+  constexpr int ROOM = SMEM_FLOATS - U * D2;
+  constexpr int EB = ROOM / (WROW + D2) < kWave ? ROOM / (WROW + D2) : kWave;
+  static_assert(EB >= kMinBatch, "LDS buffer too small for a batch of w rows");
+  float *wl = rest;
   float *yl = wl + EB * WROW;
   const float4 *w4 = reinterpret_cast<const float4 *>(w);
   float gel[L::CPL][D2];
 #pragma unroll
   for (int t = 0; t < L::CPL; ++t)
 #pragma unroll
-    for (int j = 0; j < D2; ++j) gel[t][j] = ge_s[(ul + t * kWave) * D2 + j];
+    for (int j = 0; j < D2; ++j) gel[t][j] = ge_l[(ul + t * kWave) * D2 + j];
   for (int64_t eb = e0; eb < e1; eb += EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
-    __syncthreads();  // the previous batch (or pass 1) is done with the tile memory
+    __syncthreads();  // the previous batch is done with the staged rows
     for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
       const float4 v = w4[eb * (U / 4) + i4];
       const int r = (4 * i4) / U, c = (4 * i4) % U;
@@ -448,7 +470,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
       for (int u = 0; u < U; ++u) {
         const float wv = wrow[u];
 #pragma unroll
-        for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(ge_s[u * D2 + j], wv, gy[j]);
+        for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(ge_l[u * D2 + j], wv, gy[j]);
       }
       store_row<D2>(grad_Y + (eb + lane) * D2, gy);
     }
