@@ -277,7 +277,7 @@ struct KernelTraits {
   static constexpr int kWeightLds = kWeightsInLds ? Core::NP * kWave : 1;
   // waves per SIMD the register allocation must allow
   static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
-  static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 3;
+  static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
 };
 
 // ------------------------------------------------------ tensor product fwd

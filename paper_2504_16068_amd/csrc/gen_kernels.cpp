@@ -134,31 +134,34 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
         for (const auto &e : per_path[p]) wg_needed.insert({p, e.k});
       for (const auto &pk : wg_needed)
         std::fprintf(f, "        const float wg%d_%d = W(%d) * g[%d];\n", pk.first, pk.second, pk.first, pk.second);
-      std::map<std::pair<int, int>, bool> q_init;
-      std::vector<std::pair<int, int>> q_order;
+      // Q one row i at a time: Q_ij = sum_{p,k} C_ijk wg_pk, then grad_x[i] and
+      // the env-gradient terms of that row, so only one row of Q is live.
+      std::map<int, std::map<int, std::vector<allegro::CGEntry>>> rows;  // i -> j -> entries
       for (int p : g.paths)
-        for (const auto &e : per_path[p]) {
-          const auto ij = std::make_pair(e.i, e.j);
-          const bool first = !q_init.count(ij);
-          const std::string name = "Q" + std::to_string(e.i) + "_" + std::to_string(e.j);
-          if (first) {
-            q_order.push_back(ij);
-            q_init[ij] = true;
-            std::fprintf(f, "        float %s;", name.c_str());
-          } else {
-            std::fprintf(f, "       ");
+        for (const auto &e : per_path[p]) rows[e.i][e.j].push_back(e);
+      for (const auto &row : rows) {
+        const int i = row.first, m = i - oa;
+        std::fprintf(f, "        {\n");
+        for (const auto &cell : row.second) {
+          const int j = cell.first;
+          const std::string name = "Q" + std::to_string(i) + "_" + std::to_string(j);
+          bool first = true;
+          for (const auto &e : cell.second) {
+            std::fprintf(f, "          %s%s\n", first ? "float " : "",
+                         accumulate(name, first, e.value, "wg" + std::to_string(e.path) + "_" + std::to_string(e.k)).c_str());
+            first = false;
           }
-          std::fprintf(f, " %s\n",
-                       accumulate(name, first, e.value, "wg" + std::to_string(p) + "_" + std::to_string(e.k)).c_str());
         }
-      for (const auto &ij : q_order) {
-        const int i = ij.first, j = ij.second, m = i - oa;
-        if (gx_init[m])
-          std::fprintf(f, "        gxa%d = __builtin_fmaf(Q%d_%d, env[%d], gxa%d);", m, i, j, j, m);
-        else
-          std::fprintf(f, "        gxa%d = Q%d_%d * env[%d];", m, i, j, j);
-        gx_init[m] = true;
-        std::fprintf(f, " ge[%d] = __builtin_fmaf(Q%d_%d, xa%d, ge[%d]);\n", j, i, j, m, j);
+        for (const auto &cell : row.second) {
+          const int j = cell.first;
+          if (gx_init[m])
+            std::fprintf(f, "          gxa%d = __builtin_fmaf(Q%d_%d, env[%d], gxa%d);", m, i, j, j, m);
+          else
+            std::fprintf(f, "          gxa%d = Q%d_%d * env[%d];", m, i, j, j);
+          gx_init[m] = true;
+          std::fprintf(f, " ge[%d] = __builtin_fmaf(Q%d_%d, xa%d, ge[%d]);\n", j, i, j, m, j);
+        }
+        std::fprintf(f, "        }\n");
       }
       std::fprintf(f, "      }\n");
     }
