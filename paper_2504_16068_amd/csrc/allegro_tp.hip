@@ -27,7 +27,6 @@
 #include <mutex>
 #include <new>
 #include <string>
-#include <type_traits>
 #include <vector>
 
 #include "allegro_tp.h"
@@ -162,6 +161,26 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
   for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
 }
 
+// ------------------------------------------------------------ LDS ordering
+// Orders the LDS accesses of the H waves of a workgroup without waiting for
+// their outstanding global memory operations (__syncthreads() also waits for
+// every in-flight global store, which would serialise the tile pipeline).  A
+// single wave executes its LDS operations in order, so for H == 1 only the
+// compiler needs the fences.  No kernel here relies on a barrier for global
+// memory visibility between threads.
+template <int H>
+__device__ __forceinline__ void lds_sync() {
+  if constexpr (H == 1) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  }
+}
+
 // -------------------------------------------------------------------- slabs
 // A center's per-lane rows are streamed in slabs: 64 consecutive rows of D
 // floats that are contiguous in HBM, so every slab moves with fully coalesced
@@ -173,8 +192,6 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
 template <int D>
 struct TileShape {
   static constexpr int SF4 = 16 * D;  // float4 per slab (64 rows of D floats)
-  template <int T>
-  static constexpr int per_lane() { return (T * SF4 + kWave - 1) / kWave; }
 };
 
 template <int U>
@@ -204,33 +221,60 @@ __device__ __forceinline__ int64_t tile_base(int64_t e0, int64_t e1, int64_t s0,
   }
 }
 
-template <int U, int D, int PER>
+// Cooperative tile moves by the 64 lanes of a wave; TF4 is the float4 count of
+// a full tile.  Full tiles take a path without
+// per-element predicates: predicated accesses split into basic blocks at which
+// the compiler waits for every outstanding memory operation.
+template <int U, int D, int TF4>
 __device__ __forceinline__ void tile_load(const float *__restrict__ src, float4 *tile, int64_t e0, int64_t e1,
                                           int64_t s0, int cnt, int t, int lane) {
+  constexpr int KF = TF4 / kWave, PER = (TF4 + kWave - 1) / kWave;
   int n_f4;
   const float4 *base = reinterpret_cast<const float4 *>(src) + tile_base<U, D>(e0, e1, s0, cnt, t, n_f4);
   float4 v[PER];
+  if (n_f4 == TF4) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int f = lane + kWave * k;
-    v[k] = f < n_f4 ? load_stream(base + f) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
+    for (int k = 0; k < KF; ++k) v[k] = load_stream(base + lane + kWave * k);
+    if constexpr (PER > KF) {
+      if (lane + kWave * KF < TF4) v[KF] = load_stream(base + lane + kWave * KF);
+    }
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int f = lane + kWave * k;
-    if (f < n_f4) tile[f] = v[k];
+    for (int k = 0; k < KF; ++k) tile[lane + kWave * k] = v[k];
+    if constexpr (PER > KF) {
+      if (lane + kWave * KF < TF4) tile[lane + kWave * KF] = v[KF];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int f = lane + kWave * k;
+      v[k] = f < n_f4 ? load_stream(base + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int f = lane + kWave * k;
+      if (f < n_f4) tile[f] = v[k];
+    }
   }
 }
 
-template <int U, int D, int PER>
+template <int U, int D, int TF4>
 __device__ __forceinline__ void tile_store(float *__restrict__ dst, const float4 *tile, int64_t e0, int64_t e1,
                                            int64_t s0, int cnt, int t, int lane) {
+  constexpr int KF = TF4 / kWave, PER = (TF4 + kWave - 1) / kWave;
   int n_f4;
   float4 *base = reinterpret_cast<float4 *>(dst) + tile_base<U, D>(e0, e1, s0, cnt, t, n_f4);
+  if (n_f4 == TF4) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const int f = lane + kWave * k;
-    if (f < n_f4) store_stream(tile[f], base + f);
+    for (int k = 0; k < KF; ++k) store_stream(tile[lane + kWave * k], base + lane + kWave * k);
+    if constexpr (PER > KF) {
+      if (lane + kWave * KF < TF4) store_stream(tile[lane + kWave * KF], base + lane + kWave * KF);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int f = lane + kWave * k;
+      if (f < n_f4) store_stream(tile[f], base + f);
+    }
   }
 }
 
@@ -245,36 +289,19 @@ __device__ __forceinline__ bool row_valid(int64_t e0, int64_t e1, int64_t slab, 
 }
 
 // ------------------------------------------------------------ path weights
-// The lane's weights W[p, u] of its channel u.  With few paths they sit in
-// VGPRs; with many (lmax 3, full parity: 68) they sit in an LDS column that
-// only this lane touches, read once per path and row, which frees the VGPRs
-// the lmax-3 contraction needs.
+// The lane's weights W[p, u] of its channel u, held in VGPRs.
 template <int NP>
 struct RegWeights {
   float r[NP];
-  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U, int u, float *, int) {
+  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U, int u) {
 #pragma unroll
     for (int p = 0; p < NP; ++p) r[p] = path_w[p * U + u];
   }
   __device__ __forceinline__ float operator()(int p) const { return r[p]; }
 };
 
-template <int NP>
-struct LdsWeights {
-  const float *col;
-  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U, int u, float *lds, int lane) {
-#pragma unroll 4
-    for (int p = 0; p < NP; ++p) lds[p * kWave + lane] = path_w[p * U + u];
-    col = lds + lane;
-  }
-  __device__ __forceinline__ float operator()(int p) const { return col[p * kWave]; }
-};
-
 template <class Core>
 struct KernelTraits {
-  static constexpr bool kWeightsInLds = false;
-  using Weights = typename std::conditional<kWeightsInLds, LdsWeights<Core::NP>, RegWeights<Core::NP>>::type;
-  static constexpr int kWeightLds = kWeightsInLds ? Core::NP * kWave : 1;
   // waves per SIMD the register allocation must allow
   static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
   static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
@@ -290,9 +317,8 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   using L = Lanes<U>;
   constexpr int D1 = Core::D1, D2 = Core::D2;
   constexpr int T = U > kWave ? 1 : (36 / D1 > 1 ? 36 / D1 : 1);  // slabs per tile (about 9 KB of LDS)
-  constexpr int PER = TileShape<D1>::template per_lane<T>();
-  __shared__ float4 tile[T * TileShape<D1>::SF4];
-  __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
+  constexpr int TF4 = T * TileShape<D1>::SF4;
+  __shared__ float4 tile[TF4];
   float *tile_f = reinterpret_cast<float *>(tile);
   const int lane = threadIdx.x, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
@@ -301,14 +327,14 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
     const int u = ul + t * kWave;
-    typename KernelTraits<Core>::Weights wr;
-    wr.load(path_w, U, u, w_lds, lane);
+    RegWeights<Core::NP> wr;
+    wr.load(path_w, U, u);
     float er[D2];
     load_row<D2>(env + (n * U + u) * D2, er);
     for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
       const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
-      tile_load<U, D1, PER>(x, tile, e0, e1, s0, cnt, t, lane);
-      __syncthreads();
+      tile_load<U, D1, TF4>(x, tile, e0, e1, s0, cnt, t, lane);
+      lds_sync<1>();
 #pragma unroll 1
       for (int s = 0; s < cnt; ++s) {
         if (row_valid<U>(e0, e1, s0 + s, lane)) {
@@ -321,28 +347,64 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
           for (int i = 0; i < D1; ++i) row[i] = orow[i];
         }
       }
-      __syncthreads();
-      tile_store<U, D1, PER>(out, tile, e0, e1, s0, cnt, t, lane);
-      __syncthreads();
+      lds_sync<1>();
+      tile_store<U, D1, TF4>(out, tile, e0, e1, s0, cnt, t, lane);
+      lds_sync<1>();
     }
   }
 }
 
 // ------------------------------------------------------ tensor product bwd
+// Pass 1 over channel half t: grad_x rows in place in the x tile, this lane's
+// grad_env partial sums in ge.
+template <class Core, int U, int T, int TF4>
+__device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const float *__restrict__ g,
+                                          const float *__restrict__ env, const float *__restrict__ path_w,
+                                          float *__restrict__ grad_x, float4 *tile_x, float4 *tile_g, int64_t n,
+                                          int64_t e0, int64_t e1, int64_t n_slabs, int t, int lane,
+                                          float (&ge)[Core::D2]) {
+  constexpr int D1 = Core::D1, D2 = Core::D2;
+  const int u = lane % Lanes<U>::LPE + t * kWave;
+  RegWeights<Core::NP> wr;
+  wr.load(path_w, U, u);
+  float er[D2];
+  load_row<D2>(env + (n * U + u) * D2, er);
+#pragma unroll
+  for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
+  float *tx = reinterpret_cast<float *>(tile_x);
+  const float *tg = reinterpret_cast<const float *>(tile_g);
+  for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+    const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+    tile_load<U, D1, TF4>(x, tile_x, e0, e1, s0, cnt, t, lane);
+    tile_load<U, D1, TF4>(g, tile_g, e0, e1, s0, cnt, t, lane);
+    lds_sync<1>();
+#pragma unroll 1
+    for (int s = 0; s < cnt; ++s) {
+      if (row_valid<U>(e0, e1, s0 + s, lane)) {
+        // x row in, grad_x row out, in place in the LDS tile
+        float *row = tx + (s * kWave + lane) * D1;
+        Core::bwd(row, er, wr, tg + (s * kWave + lane) * D1, row, ge);
+      }
+    }
+    lds_sync<1>();
+    tile_store<U, D1, TF4>(grad_x, tile_x, e0, e1, s0, cnt, t, lane);
+    lds_sync<1>();
+  }
+}
+
 template <class Core, int U>
 __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kBwdOccupancy))) void tp_backward_kernel(
-    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
-    const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
-    const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
-    float *__restrict__ grad_w, float *__restrict__ grad_Y) {
+        const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+        const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
+        const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
+        float *__restrict__ grad_w, float *__restrict__ grad_Y) {
   using L = Lanes<U>;
   constexpr int D1 = Core::D1, D2 = Core::D2;
   constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
-  constexpr int PER = TileShape<D1>::template per_lane<T>();
   constexpr int TILE_F4 = T * TileShape<D1>::SF4;
   // One LDS buffer serves both passes: the x and g tiles in pass 1; in pass 2
   // grad_env[n] of all channels followed by staged w and Y rows (at least
-  // kMinBatch edges) or, with several lane groups, their partial sums.
+  // kMinBatch edges) or by the lane groups' partial sums.
   constexpr int WROW = U + 1;  // padded w row: per-lane row reads hit distinct banks
   constexpr int kMinBatch = 8;
   constexpr int P1_FLOATS = 2 * TILE_F4 * 4;
@@ -351,12 +413,9 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   constexpr int P2_FLOATS = U * D2 + (PART_FLOATS > ROWS_FLOATS ? PART_FLOATS : ROWS_FLOATS);
   constexpr int SMEM_FLOATS = P1_FLOATS > P2_FLOATS ? P1_FLOATS : P2_FLOATS;
   __shared__ float4 smem[(SMEM_FLOATS + 3) / 4];
-  __shared__ float w_lds[KernelTraits<Core>::kWeightLds];
   float4 *tile_x = smem, *tile_g = smem + TILE_F4;
-  float *tx = reinterpret_cast<float *>(tile_x);
-  const float *tg = reinterpret_cast<const float *>(tile_g);
   float *ge_l = reinterpret_cast<float *>(smem);  // pass 2: grad_env[n, :, :]
-  float *rest = ge_l + U * D2;                    // pass 2: group partials, then w / Y rows
+  float *rest = ge_l + U * D2;                    // partial sums, then pass-2 w / Y rows
   const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
@@ -366,38 +425,16 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
     const int u = ul + t * kWave;
-    typename KernelTraits<Core>::Weights wr;
-    wr.load(path_w, U, u, w_lds, lane);
-    float er[D2], ge[D2];
-    load_row<D2>(env + (n * U + u) * D2, er);
-#pragma unroll
-    for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
-    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
-      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
-      tile_load<U, D1, PER>(x, tile_x, e0, e1, s0, cnt, t, lane);
-      tile_load<U, D1, PER>(g, tile_g, e0, e1, s0, cnt, t, lane);
-      __syncthreads();
-#pragma unroll 1
-      for (int s = 0; s < cnt; ++s) {
-        if (row_valid<U>(e0, e1, s0 + s, lane)) {
-          // x row in, grad_x row out, in place in the LDS tile
-          float *row = tx + (s * kWave + lane) * D1;
-          Core::bwd(row, er, wr, tg + (s * kWave + lane) * D1, row, ge);
-        }
-      }
-      __syncthreads();
-      tile_store<U, D1, PER>(grad_x, tile_x, e0, e1, s0, cnt, t, lane);
-      __syncthreads();
-    }
-    // grad_env of this channel half goes straight to its output (the tile loop's
-    // last barrier has passed, so the LDS buffer is free for the group partials)
+    float ge[D2];
+    bwd_pass1<Core, U, T, TILE_F4>(x, g, env, path_w, grad_x, tile_x, tile_g, n, e0, e1, n_slabs, t, lane, ge);
+    // grad_env of this channel half goes straight to its output
     if constexpr (L::G == 1) {
       store_row<D2>(grad_env + (n * U + u) * D2, ge);
     } else {
-      // combine the lane groups in a fixed order
+      // combine the lane groups in a fixed order (the tile loop is done with the buffer)
 #pragma unroll
       for (int j = 0; j < D2; ++j) rest[lane * D2 + j] = ge[j];
-      __syncthreads();
+      lds_sync<1>();
       if (grp == 0) {
         float acc[D2];
 #pragma unroll
@@ -409,7 +446,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
       }
     }
   }
-  __syncthreads();
+  lds_sync<1>();
   // Stage grad_env[n] in LDS for pass 2.  Every lane copies back only values it
   // stored itself, so program order alone makes them visible to it.
   if (grp == 0) {
@@ -421,7 +458,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
       for (int j = 0; j < D2; ++j) ge_l[(ul + t * kWave) * D2 + j] = v[j];
     }
   }
-  __syncthreads();
+  lds_sync<1>();
 
   // Pass 2: the embedding's VJP through grad_env, in batches of EB edges whose w and
   // Y rows are first staged into the (now free) tile memory with one round of
@@ -443,7 +480,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
     for (int j = 0; j < D2; ++j) gel[t][j] = ge_l[(ul + t * kWave) * D2 + j];
   for (int64_t eb = e0; eb < e1; eb += EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
-    __syncthreads();  // the previous batch is done with the staged rows
+    lds_sync<1>();  // the previous batch is done with the staged rows
     for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
       const float4 v = w4[eb * (U / 4) + i4];
       const int r = (4 * i4) / U, c = (4 * i4) % U;
@@ -451,7 +488,7 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
       dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
     }
     for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
-    __syncthreads();
+    lds_sync<1>();
     for (int k = grp; k < cnt; k += L::G) {
 #pragma unroll
       for (int t = 0; t < L::CPL; ++t) {

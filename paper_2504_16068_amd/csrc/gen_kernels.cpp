@@ -12,7 +12,7 @@
 //        ge[j]  += sum_i Q_ij x[i]             (accumulated across edges)
 // which is the tensor product and its VJP with respect to x and env, written
 // per pair of input blocks so that at most one block of temporaries is live.
-// W is any accessor with W(p) = the lane's weight of path p (registers or LDS).
+// W is any accessor with W(p) = the lane's weight of path p.
 //
 // Usage: gen_kernels <output.inc>
 #include <cstdio>
@@ -113,12 +113,13 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   // Emitted per x irrep a: its x values are read once at the start of the
   // section and its grad_x values are written once at the end, so x and gx may
   // be the same row (in-place) and only one block of gx accumulators is live.
+  const int nx = int(t.x_irreps.size());
   std::fprintf(f,
                "  template <class WT>\n"
                "  static __device__ __forceinline__ void bwd(const float *x, const float *__restrict__ env,\n"
                "                                             const WT &W, const float *__restrict__ g,\n"
                "                                             float *gx, float *__restrict__ ge) {\n");
-  for (int a = 0; a < int(t.x_irreps.size()); ++a) {
+  for (int a = 0; a < nx; ++a) {
     const int la = t.x_irreps[a].l, oa = t.x_off[a], da = 2 * la + 1;
     std::fprintf(f, "    { // x block %d (l=%d)\n", a, la);
     for (int m = 0; m < da; ++m) std::fprintf(f, "      const float xa%d = x[%d];\n", m, oa + m);
@@ -167,9 +168,6 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
     }
     for (int m = 0; m < da; ++m)
       std::fprintf(f, "      gx[%d] = %s;\n", oa + m, gx_init[m] ? ("gxa" + std::to_string(m)).c_str() : "0.0f");
-    // keep the machine scheduler from merging sections (it would hoist every
-    // section's loads and spill); one section's temporaries are live at a time
-    std::fprintf(f, "      __builtin_amdgcn_sched_barrier(0);\n");
     std::fprintf(f, "    }\n");
   }
   std::fprintf(f, "  }\n};\n\n");
