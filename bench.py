@@ -136,6 +136,35 @@ def copy_bandwidth(torch, dev, n_bytes=4 << 30, reps=10):
     return 2 * n_bytes / sec / 1e9
 
 
+def time_harmonics(torch, at, plan, graph, dev, reps):
+    """Timings of the fp64 harmonics of the edge vectors and their Cartesian VJP (outside the step).
+
+    Algorithmic bytes per edge: forward reads r (24 B) and writes Y (4 d2 B); the
+    backward reads r and grad_Y and writes grad_r (24 B).
+    """
+    e, d2 = graph.n_edges, plan.d2
+    vec = torch.from_numpy(graph.vec).to(dev)
+    y = torch.empty((e, d2), device=dev)
+    gy = torch.ones((e, d2), device=dev)
+    gv = torch.empty((e, 3), device=dev, dtype=torch.float64)
+    calls = {"sh_forward": lambda: at.allegro_sh_forward(plan, vec, Y=y),
+             "sh_backward": lambda: at.allegro_sh_backward(plan, vec, gy, grad_vec=gv)}
+    nbytes = {"sh_forward": e * (24 + 4 * d2), "sh_backward": e * (48 + 4 * d2)}
+    res = {}
+    for name, fn in calls.items():
+        fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        res[name] = {"ms": ms, "hbm_algorithmic_GBps": nbytes[name] / (ms / 1e3) / 1e9}
+    del vec, y, gy, gv
+    return res
+
+
 def cpu_baseline(graph, host_inputs, max_edges=8192):
     """Time the fp64 oracle (one thread) on a prefix of whole center segments."""
     from threadpoolctl import threadpool_limits
@@ -227,6 +256,7 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     value = n_edges / (ms_per_step / 1e3)
 
+    harmonics = time_harmonics(torch, at, plan, graph, dev, args.steps)
     algo = algorithmic_bytes(cfg, n_atoms, n_edges)
     bwd_s = per_kernel_ms["tp_backward"] / 1e3
     achieved = algo["tp_backward"] / bwd_s / 1e9
@@ -268,6 +298,7 @@ def main():
             "algorithmic_bytes_per_launch": algo["tp_backward"],
             "frac_of_measured_copy": achieved / copy_gbps,
         },
+        "edge_harmonics": harmonics,
         "kernel_source_digest": kernel_source_digest(),
     }
     del x, w, g, out, grads, env

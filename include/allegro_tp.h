@@ -131,6 +131,22 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
                         float *grad_x, float *grad_env, float *grad_w, float *grad_Y,
                         void *stream);
 
+/* Real spherical harmonics of the edge vectors, the embedding input of the
+ * environment sum (Appendix "Mixed-Precision Architecture": embedded in fp64,
+ * then cast to fp32): Y[E][d2] = fl32(Y^l_m(vec_e)), l = 0..lmax, m = -l..l,
+ * component normalisation sum_m (Y^l_m)^2 = 2l + 1, real basis with l = 1
+ * ordered (y, z, x).  vec[E][3] is fp64 (r_ij = r_j - r_i); Y depends on its
+ * direction only.  A zero vector has no direction and yields NaN. */
+int allegro_sh_forward(const allegro_tp_plan *plan, int64_t E, const double *vec, float *Y, void *stream);
+
+/* VJP of allegro_sh_forward, in fp64 as the forward: grad_vec[e][k] =
+ * sum_j grad_Y[e][j] dY_j/dvec_e[k], with grad_Y[E][d2] fp32 (as produced by
+ * allegro_tp_backward) and grad_vec[E][3] fp64.  Summing grad_vec into the two
+ * atoms of each edge (minus at the center, plus at the neighbour) gives that
+ * loss's gradient with respect to positions through the harmonics. */
+int allegro_sh_backward(const allegro_tp_plan *plan, int64_t E, const double *vec, const float *grad_Y,
+                        double *grad_vec, void *stream);
+
 /* Message of the last failed call on this thread ("" if none). */
 const char *allegro_last_error(void);
 

@@ -19,6 +19,8 @@ from .binding import (  # noqa: F401
     Plan,
     allegro_env_embed,
     allegro_last_error,
+    allegro_sh_backward,
+    allegro_sh_forward,
     allegro_tp_backward,
     allegro_tp_forward,
     allegro_tp_plan_create,

@@ -27,7 +27,8 @@ ALLEGRO_VALIDATE = 4
 
 EXPORTED = (
     "allegro_tp_plan_create", "allegro_tp_plan_destroy", "allegro_tp_plan_query", "allegro_tp_plan_cg",
-    "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_last_error",
+    "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_sh_forward", "allegro_sh_backward",
+    "allegro_last_error",
 )
 
 
@@ -56,6 +57,8 @@ def _load() -> ctypes.CDLL:
     lib.allegro_env_embed.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp]
     lib.allegro_tp_forward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp]
     lib.allegro_tp_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.allegro_sh_forward.argtypes = [vp, i64, vp, vp, vp]
+    lib.allegro_sh_backward.argtypes = [vp, i64, vp, vp, vp, vp]
     lib.allegro_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
         if name != "allegro_last_error":
@@ -214,3 +217,32 @@ def allegro_tp_backward(plan: Plan, row_ptr, x, env, path_w, grad_out, w, Y, out
                                     _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw), _ptr(gy),
                                     _stream(stream, dev)))
     return gx, genv, gw, gy
+
+
+def allegro_sh_forward(plan: Plan, vec, Y=None, stream=None):
+    """Y [E, d2] float32 from edge vectors vec [E, 3] float64."""
+    import torch
+
+    dev = vec.device
+    e = vec.shape[0]
+    _need(vec, "vec", (e, 3), torch.float64, dev)
+    if Y is None:
+        Y = torch.empty((e, plan.d2), device=dev, dtype=torch.float32)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    _check(_lib.allegro_sh_forward(plan.handle, e, _ptr(vec), _ptr(Y), _stream(stream, dev)))
+    return Y
+
+
+def allegro_sh_backward(plan: Plan, vec, grad_Y, grad_vec=None, stream=None):
+    """grad_vec [E, 3] float64 from vec [E, 3] float64 and grad_Y [E, d2] float32."""
+    import torch
+
+    dev = vec.device
+    e = vec.shape[0]
+    _need(vec, "vec", (e, 3), torch.float64, dev)
+    _need(grad_Y, "grad_Y", (e, plan.d2), torch.float32, dev)
+    if grad_vec is None:
+        grad_vec = torch.empty((e, 3), device=dev, dtype=torch.float64)
+    _need(grad_vec, "grad_vec", (e, 3), torch.float64, dev)
+    _check(_lib.allegro_sh_backward(plan.handle, e, _ptr(vec), _ptr(grad_Y), _ptr(grad_vec), _stream(stream, dev)))
+    return grad_vec

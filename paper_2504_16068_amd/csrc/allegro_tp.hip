@@ -514,6 +514,95 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
   }
 }
 
+// ------------------------------------------------------ spherical harmonics
+// Real harmonics of an edge vector r, component normalisation, as Cartesian
+// polynomials of the unit vector u = r/|r| (l <= 3), evaluated in fp64 with
+// forward-mode dual numbers so that the same code yields dY/dr exactly.
+struct Dual {
+  double v, g[3];  // value and gradient with respect to r
+};
+
+__device__ __forceinline__ Dual dmul(const Dual &a, const Dual &b) {
+  return {a.v * b.v, {a.v * b.g[0] + a.g[0] * b.v, a.v * b.g[1] + a.g[1] * b.v, a.v * b.g[2] + a.g[2] * b.v}};
+}
+__device__ __forceinline__ Dual dscale(double c, const Dual &a) { return {c * a.v, {c * a.g[0], c * a.g[1], c * a.g[2]}}; }
+__device__ __forceinline__ Dual dadd(const Dual &a, const Dual &b) {
+  return {a.v + b.v, {a.g[0] + b.g[0], a.g[1] + b.g[1], a.g[2] + b.g[2]}};
+}
+__device__ __forceinline__ Dual dsub(const Dual &a, const Dual &b) {
+  return {a.v - b.v, {a.g[0] - b.g[0], a.g[1] - b.g[1], a.g[2] - b.g[2]}};
+}
+__device__ __forceinline__ Dual dconst(double c) { return {c, {0.0, 0.0, 0.0}}; }
+
+// Y[0 .. (LMAX+1)^2) of the vector (rx, ry, rz).
+template <int LMAX>
+__device__ __forceinline__ void real_sh(double rx, double ry, double rz, Dual (&Yd)[(LMAX + 1) * (LMAX + 1)]) {
+  const double n2 = rx * rx + ry * ry + rz * rz;
+  const double inv = 1.0 / sqrt(n2);  // d(1/|r|)/dr = -r / |r|^3
+  const double inv3 = inv * inv * inv;
+  const Dual s = {inv, {-rx * inv3, -ry * inv3, -rz * inv3}};
+  const Dual x = dmul({rx, {1.0, 0.0, 0.0}}, s), y = dmul({ry, {0.0, 1.0, 0.0}}, s), z = dmul({rz, {0.0, 0.0, 1.0}}, s);
+  Yd[0] = dconst(1.0);
+  if constexpr (LMAX >= 1) {
+    const double c1 = sqrt(3.0);
+    Yd[1] = dscale(c1, y);
+    Yd[2] = dscale(c1, z);
+    Yd[3] = dscale(c1, x);
+  }
+  if constexpr (LMAX >= 2) {
+    const double c15 = sqrt(15.0), c5 = sqrt(5.0);
+    const Dual xx = dmul(x, x), yy = dmul(y, y), zz = dmul(z, z);
+    Yd[4] = dscale(c15, dmul(x, y));
+    Yd[5] = dscale(c15, dmul(y, z));
+    Yd[6] = dscale(0.5 * c5, dsub(dscale(3.0, zz), dconst(1.0)));
+    Yd[7] = dscale(c15, dmul(x, z));
+    Yd[8] = dscale(0.5 * c15, dsub(xx, yy));
+    if constexpr (LMAX >= 3) {
+      const double a = sqrt(70.0) / 4.0, b = sqrt(105.0), c = sqrt(42.0) / 4.0, d = sqrt(7.0) / 2.0;
+      const Dual z5m1 = dsub(dscale(5.0, zz), dconst(1.0));
+      Yd[9] = dscale(a, dmul(y, dsub(dscale(3.0, xx), yy)));
+      Yd[10] = dscale(b, dmul(dmul(x, y), z));
+      Yd[11] = dscale(c, dmul(y, z5m1));
+      Yd[12] = dscale(d, dmul(z, dsub(dscale(5.0, zz), dconst(3.0))));
+      Yd[13] = dscale(c, dmul(x, z5m1));
+      Yd[14] = dscale(0.5 * b, dmul(z, dsub(xx, yy)));
+      Yd[15] = dscale(a, dmul(x, dsub(xx, dscale(3.0, yy))));
+    }
+  }
+}
+
+template <int LMAX>
+__global__ __launch_bounds__(256) void sh_forward_kernel(int64_t E, const double *__restrict__ vec,
+                                                         float *__restrict__ Y) {
+  constexpr int D2 = (LMAX + 1) * (LMAX + 1);
+  const int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  Dual Yd[D2];
+  real_sh<LMAX>(vec[3 * e], vec[3 * e + 1], vec[3 * e + 2], Yd);
+#pragma unroll
+  for (int j = 0; j < D2; ++j) Y[e * D2 + j] = float(Yd[j].v);
+}
+
+template <int LMAX>
+__global__ __launch_bounds__(256) void sh_backward_kernel(int64_t E, const double *__restrict__ vec,
+                                                          const float *__restrict__ grad_Y,
+                                                          double *__restrict__ grad_vec) {
+  constexpr int D2 = (LMAX + 1) * (LMAX + 1);
+  const int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= E) return;
+  Dual Yd[D2];
+  real_sh<LMAX>(vec[3 * e], vec[3 * e + 1], vec[3 * e + 2], Yd);
+  double gr[3] = {0.0, 0.0, 0.0};
+#pragma unroll
+  for (int j = 0; j < D2; ++j) {
+    const double gy = double(grad_Y[e * D2 + j]);
+#pragma unroll
+    for (int k = 0; k < 3; ++k) gr[k] += gy * Yd[j].g[k];
+  }
+#pragma unroll
+  for (int k = 0; k < 3; ++k) grad_vec[3 * e + k] = gr[k];
+}
+
 // ------------------------------------------------------------- CSR check
 __global__ void zero_word_kernel(int *word) { *word = 0; }
 
@@ -783,6 +872,48 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
   if (!k.bwd) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
   k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y);
   return after_launch("allegro_tp_backward");
+}
+
+// One edge per thread in 256-thread blocks; the grid's x extent stays below 2^31.
+constexpr int64_t kMaxShEdges = (int64_t(1) << 31) * 255;
+
+int allegro_sh_forward(const allegro_tp_plan *plan, int64_t E, const double *vec, float *Y, void *stream) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (E < 0) return fail(ALLEGRO_E_INVALID, "negative size (E=%lld)", (long long)E);
+  if (E == 0) return ALLEGRO_OK;
+  if (E > kMaxShEdges) return fail(ALLEGRO_E_INVALID, "E=%lld exceeds the grid limit", (long long)E);
+  int rc;
+  if ((rc = check_tensor(vec, "vec")) || (rc = check_tensor(Y, "Y"))) return rc;
+  const unsigned blocks = unsigned((E + 255) / 256);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (plan->lmax) {
+    case 1: hipLaunchKernelGGL(sh_forward_kernel<1>, dim3(blocks), dim3(256), 0, s, E, vec, Y); break;
+    case 2: hipLaunchKernelGGL(sh_forward_kernel<2>, dim3(blocks), dim3(256), 0, s, E, vec, Y); break;
+    case 3: hipLaunchKernelGGL(sh_forward_kernel<3>, dim3(blocks), dim3(256), 0, s, E, vec, Y); break;
+    default: return fail(ALLEGRO_E_UNSUPPORTED, "lmax=%d", plan->lmax);
+  }
+  return after_launch("allegro_sh_forward");
+}
+
+int allegro_sh_backward(const allegro_tp_plan *plan, int64_t E, const double *vec, const float *grad_Y,
+                        double *grad_vec, void *stream) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (E < 0) return fail(ALLEGRO_E_INVALID, "negative size (E=%lld)", (long long)E);
+  if (E == 0) return ALLEGRO_OK;
+  if (E > kMaxShEdges) return fail(ALLEGRO_E_INVALID, "E=%lld exceeds the grid limit", (long long)E);
+  int rc;
+  if ((rc = check_tensor(vec, "vec")) || (rc = check_tensor(grad_Y, "grad_Y")) ||
+      (rc = check_tensor(grad_vec, "grad_vec")))
+    return rc;
+  const unsigned blocks = unsigned((E + 255) / 256);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  switch (plan->lmax) {
+    case 1: hipLaunchKernelGGL(sh_backward_kernel<1>, dim3(blocks), dim3(256), 0, s, E, vec, grad_Y, grad_vec); break;
+    case 2: hipLaunchKernelGGL(sh_backward_kernel<2>, dim3(blocks), dim3(256), 0, s, E, vec, grad_Y, grad_vec); break;
+    case 3: hipLaunchKernelGGL(sh_backward_kernel<3>, dim3(blocks), dim3(256), 0, s, E, vec, grad_Y, grad_vec); break;
+    default: return fail(ALLEGRO_E_UNSUPPORTED, "lmax=%d", plan->lmax);
+  }
+  return after_launch("allegro_sh_backward");
 }
 
 const char *allegro_last_error(void) { return g_last_error.c_str(); }

@@ -116,6 +116,13 @@ def test_entry_points_reject_bad_arguments_before_any_launch():
     assert rc == binding.ALLEGRO_E_INVALID and "grad_Y" in msg
     rc, msg = _err(lib.allegro_env_embed, h, 3, 5, ok_rp, ok_ptr, None, ok_ptr, None)
     assert rc == binding.ALLEGRO_E_INVALID and "Y is NULL" in msg
+    rc, msg = _err(lib.allegro_sh_forward, h, 4, bad_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "vec" in msg
+    rc, msg = _err(lib.allegro_sh_backward, h, -1, ok_ptr, ok_ptr, ok_ptr, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "negative" in msg
+    rc, msg = _err(lib.allegro_sh_backward, h, 4, ok_ptr, ok_ptr, None, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "grad_vec is NULL" in msg
+    assert lib.allegro_sh_forward(h, 0, None, None, None) == binding.ALLEGRO_OK
     # empty problem: successful no-op
     for fn, nargs in ((lib.allegro_env_embed, 5), (lib.allegro_tp_forward, 6), (lib.allegro_tp_backward, 12)):
         rc = fn(h, 0, 0, *([None] * (nargs - 1)), None)

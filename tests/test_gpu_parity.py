@@ -235,3 +235,61 @@ def _sampled_check(at, name, n_samples=24):
 @pytest.mark.parametrize("name", ["headline", "high_order", "large"])
 def test_full_size_sampled_segments(at, name):
     _sampled_check(at, name)
+
+
+# ------------------------------------------------ spherical harmonics of edges
+
+def _sh_vectors(n, seed):
+    rng = np.random.default_rng(seed)
+    v = rng.standard_normal((n, 3)) * rng.uniform(0.3, 6.0, (n, 1))
+    # axis-aligned and near-polar directions, tiny and large lengths
+    special = np.array([[0, 0, 1], [0, 0, -1], [1, 0, 0], [0, -1, 0], [1e-9, 0, 1], [0, 1e-12, -3],
+                        [1e-3, 2e-3, 1e-3], [4e2, -3e2, 5e2]], dtype=np.float64)
+    return np.concatenate([special, v])
+
+
+@pytest.mark.parametrize("lmax", [1, 2, 3])
+def test_sh_forward_and_backward(at, lmax):
+    from oracle import sh as osh
+
+    _note(f"[gpu] harmonics lmax={lmax}")
+    plan = _plan(at, lmax, 64, True)
+    vec = _sh_vectors(5000, 40 + lmax)
+    d2 = (lmax + 1) ** 2
+    gy = np.random.default_rng(lmax).standard_normal((len(vec), d2)).astype(np.float32)
+    vd = _t(vec)
+    y = at.allegro_sh_forward(plan, vd).cpu().numpy()
+    gv = at.allegro_sh_backward(plan, vd, _t(gy)).cpu().numpy()
+    ref_y = osh.sh_real_all(lmax, vec)
+    # evaluated in fp64 and rounded once to fp32: within one fp32 rounding of the fp64 value
+    assert np.all(np.abs(y - ref_y) <= 2.0 ** -23 * np.abs(ref_y) + 1e-12)
+    ref_g = osh.sh_backward(lmax, vec, gy)
+    err = block_rel_err(gv, ref_g)
+    _note(f"harmonics lmax={lmax}: grad_vec err={err:.2e}")
+    assert err <= 1e-7
+
+
+def test_sh_headline_vectors_sampled(at):
+    from oracle import sh as osh
+
+    graph = workloads.make_graph("headline")
+    _note(f"[gpu] harmonics of the headline edges: E={graph.n_edges}")
+    plan = _plan(at, 2, 64, True)
+    vd = _t(graph.vec)
+    y = at.allegro_sh_forward(plan, vd)
+    gy = torch.randn((graph.n_edges, 9), generator=torch.Generator(device=DEV).manual_seed(3), device=DEV)
+    gv = at.allegro_sh_backward(plan, vd, gy)
+    torch.cuda.synchronize()
+    yh, gvh, vec = y.cpu().numpy(), gv.cpu().numpy(), graph.vec
+    # every edge: sum_m Y_lm^2 = 2l + 1 and r . grad_vec = 0 (Y depends on the direction only)
+    for l in range(3):
+        norm = np.sum(yh[:, l * l:(l + 1) ** 2].astype(np.float64) ** 2, axis=1)
+        assert np.max(np.abs(norm - (2 * l + 1))) <= 1e-6 * (2 * l + 1)
+    radial = np.abs(np.sum(vec * gvh, axis=1))
+    assert np.max(radial) <= 1e-12 * np.max(np.abs(gvh) * np.linalg.norm(vec, axis=1, keepdims=True))
+    # sampled edges against the oracle
+    idx = np.random.default_rng(9).integers(0, graph.n_edges, 4096)
+    ref_y = osh.sh_real_all(2, vec[idx])
+    assert np.all(np.abs(yh[idx] - ref_y) <= 2.0 ** -23 * np.abs(ref_y) + 1e-12)
+    ref_g = osh.sh_backward(2, vec[idx], gy.cpu().numpy()[idx])
+    assert block_rel_err(gvh[idx], ref_g) <= 1e-7

@@ -80,3 +80,34 @@ def test_wigner_properties():
         np.testing.assert_allclose(d12, d1 @ d2, atol=1e-11)
     perm = np.eye(3)[[1, 2, 0]]  # (x, y, z) -> (y, z, x)
     np.testing.assert_allclose(wigner.wigner_d_real(1, r1), perm @ r1 @ perm.T, atol=1e-12)
+
+
+def test_gradient_closed_form_l1_and_scale_invariance():
+    rng = np.random.default_rng(4)
+    v = rng.standard_normal((30, 3)) * rng.uniform(0.5, 5.0, (30, 1))
+    grad = sh.sh_real_all_grad(2, v)
+    r = np.linalg.norm(v, axis=1)
+    u = v / r[:, None]
+    # l = 1: Y = sqrt3 (y, z, x) / |r|  ->  dY/dr = sqrt3 (e_a - u_a u) / |r|
+    for col, axis in ((1, 1), (2, 2), (3, 0)):
+        expect = sqrt(3) * (np.eye(3)[axis][None, :] - u[:, axis:axis + 1] * u) / r[:, None]
+        np.testing.assert_allclose(grad[:, col, :], expect, atol=1e-9)
+    # Y is homogeneous of degree 0, so r . grad Y = 0 for every component
+    np.testing.assert_allclose(np.einsum("ek,ejk->ej", v, grad), 0.0, atol=1e-9)
+    # the scalar component is constant
+    np.testing.assert_allclose(grad[:, 0, :], 0.0, atol=1e-12)
+
+
+def test_gradient_equivariance_and_vjp():
+    rng = np.random.default_rng(5)
+    rot = wigner.random_rotation(rng)
+    v = rng.standard_normal((20, 3))
+    lmax = 3
+    # Y(R r) = D Y(r)  =>  J(R r) R = D J(r)   (J = dY/dr)
+    blocks = [(l, 1 if l % 2 == 0 else -1) for l in range(lmax + 1)]
+    d = wigner.wigner_d_blocks(blocks, rot)
+    j_rot = sh.sh_real_all_grad(lmax, v @ rot.T)
+    j = sh.sh_real_all_grad(lmax, v)
+    np.testing.assert_allclose(np.einsum("ejk,kl->ejl", j_rot, rot), np.einsum("ij,ejk->eik", d, j), atol=1e-8)
+    gy = rng.standard_normal((20, 16))
+    np.testing.assert_allclose(sh.sh_backward(lmax, v, gy), np.einsum("ej,ejk->ek", gy, j), atol=1e-12)
