@@ -17,6 +17,9 @@ center i, channels u, irreps (l, p)):
   and the VJP of the embedding through grad_env:
       grad_w[e, u] = sum_j grad_env[c(e), u, j] Y[e, j]
       grad_Y[e, j] = sum_u grad_env[c(e), u, j] w[e, u]
+  and, for training (the paper leaves its kernels to future work, §II.D), the
+  gradient of the path weights, a reduction over every edge:
+      grad_W[p, u] = sum_e sum_{(i, j, k) in p} C_ijk x[e, u, i] env[c(e), u, j] g[e, u, k]
 
 Segments: edge e belongs to center n iff row_ptr[n] <= e < row_ptr[n+1]; an
 empty segment gives env = 0 and grad_env = 0.
@@ -223,3 +226,34 @@ class TensorProduct:
                     grad_w[e, u] += grad_env[n, u, j] * yv[e, j]
                     grad_y[e, j] += grad_env[n, u, j] * wv[e, u]
         return grad_x, grad_env, grad_w, grad_y
+
+    # ---- path-weight gradient (training)
+    def path_weight_grad(self, row_ptr, x, env, g) -> np.ndarray:
+        """grad_W [P, U]: out is linear in W, so this is sum_e <g[e, u, block c], path p's contraction>."""
+        x64, env64, g64 = _f64(x), _f64(env), _f64(g)
+        c = centers_of_edges(row_ptr)
+        n_edges, n_ch, _ = x64.shape
+        grad = np.zeros((self.n_paths, n_ch))
+        for s in range(0, n_edges, _CHUNK):
+            t = min(s + _CHUNK, n_edges)
+            xe, ee, ge = x64[s:t], env64[c[s:t]], g64[s:t]
+            for p, (a, b, cc) in enumerate(self.paths):
+                grad[p] += np.einsum("eui,euj,euk,ijk->u", xe[:, :, self.x_slices[a]], ee[:, :, self.env_slices[b]],
+                                     ge[:, :, self.x_slices[cc]], self.blocks[p], optimize=True)
+        return grad
+
+    def path_weight_grad_loops(self, row_ptr, x, env, g) -> np.ndarray:
+        x64, env64, g64 = _f64(x), _f64(env), _f64(g)
+        c = centers_of_edges(row_ptr)
+        n_edges, n_ch, _ = x64.shape
+        grad = np.zeros((self.n_paths, n_ch))
+        for e in range(n_edges):
+            n = c[e]
+            for u in range(n_ch):
+                for p, (a, b, cc) in enumerate(self.paths):
+                    blk = self.blocks[p]
+                    oa, ob, oc = self.x_slices[a].start, self.env_slices[b].start, self.x_slices[cc].start
+                    for m1, m2, m3 in zip(*np.nonzero(blk)):
+                        grad[p, u] += (blk[m1, m2, m3] * x64[e, u, oa + m1] * env64[n, u, ob + m2]
+                                       * g64[e, u, oc + m3])
+        return grad

@@ -9,7 +9,9 @@
   over sqrt 3, 1o x 1o -> 1e the cross product over sqrt 2;
 * the VJP: exact adjoint identities of a bilinear map and central finite
   differences through x, env, w and Y;
-* the embedding: brute-force loops, empty segments, and the fp32 replay.
+* the embedding: brute-force loops, empty segments, and the fp32 replay;
+* the path-weight gradient: out is linear in W, so each grad_W[p, u] equals
+  <g, out> with W the one-hot e_pu (the forward, pinned above).
 """
 
 from math import sqrt
@@ -172,3 +174,26 @@ def test_backward_finite_differences():
         fd_y = (loss(x, w, y + h * vy) - loss(x, w, y - h * vy)) / (2 * h)
         for fd, an in ((fd_x, np.sum(gx * vx)), (fd_w, np.sum(gw * vw)), (fd_y, np.sum(gy * vy))):
             assert abs(fd - an) <= 1e-8 * max(1.0, abs(an)), (fd, an)
+
+
+@pytest.mark.parametrize("lmax,full,n_ch", CASES)
+def test_path_weight_grad(lmax, full, n_ch):
+    """grad_W against the forward: out is linear in W, so grad_W[p, u] = <g, out(W = e_pu)>."""
+    row_ptr, _, x, w, W, g, y = _problem(lmax, full, n_ch, seed=12)
+    t = tp.TensorProduct(lmax, full)
+    env = tp.env_embed(row_ptr, w, y)
+    gW = t.path_weight_grad(row_ptr, x, env, g)
+    assert gW.shape == (t.n_paths, n_ch)
+    onehot = np.zeros_like(W)
+    for p in range(t.n_paths):
+        for u in range(n_ch):
+            onehot[p, u] = 1.0
+            ref = np.sum(g * t.forward(row_ptr, x, env, onehot))
+            onehot[p, u] = 0.0
+            assert abs(gW[p, u] - ref) <= 1e-11 * (abs(ref) + 1), (p, u)
+    # the loop form agrees; a segment-free edge set gives zero
+    small = row_ptr[:4] if lmax == 3 else row_ptr
+    ne = int(small[-1])
+    loops = t.path_weight_grad_loops(small, x[:ne], env, g[:ne])
+    assert np.abs(loops - t.path_weight_grad(small, x[:ne], env, g[:ne])).max() <= 1e-12 * (np.abs(loops).max() + 1)
+    assert not t.path_weight_grad(np.zeros(3, np.int64), x[:0], env[:2], g[:0]).any()
