@@ -165,6 +165,29 @@ def time_harmonics(torch, at, plan, graph, dev, reps):
     return res
 
 
+def time_training_backward(torch, at, plan, inputs, grads, per_kernel_ms, reps):
+    """The training backward (also grad_path_w), timed outside the step: the
+    whole call, and the extra time over the inference backward."""
+    rp, x, env, pw, g, w, y = inputs
+    ws = torch.empty(at.allegro_tp_backward_workspace(plan, rp.numel() - 1), dtype=torch.uint8, device=x.device)
+    outs = (*grads, torch.empty_like(pw))
+
+    def call():
+        at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, outs=outs, workspace=ws)
+
+    call()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        call()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del ws
+    return {"ms": ms, "extra_over_backward_ms": ms - per_kernel_ms["tp_backward"],
+            "workspace_bytes": at.allegro_tp_backward_workspace(plan, rp.numel() - 1)}
+
+
 def cpu_baseline(graph, host_inputs, max_edges=8192):
     """Time the fp64 oracle (one thread) on a prefix of whole center segments."""
     from threadpoolctl import threadpool_limits
@@ -257,6 +280,7 @@ def main():
     value = n_edges / (ms_per_step / 1e3)
 
     harmonics = time_harmonics(torch, at, plan, graph, dev, args.steps)
+    training = time_training_backward(torch, at, plan, (rp, x, env, pw, g, w, y), grads, per_kernel_ms, args.steps)
     algo = algorithmic_bytes(cfg, n_atoms, n_edges)
     bwd_s = per_kernel_ms["tp_backward"] / 1e3
     achieved = algo["tp_backward"] / bwd_s / 1e9
@@ -299,6 +323,7 @@ def main():
             "frac_of_measured_copy": achieved / copy_gbps,
         },
         "edge_harmonics": harmonics,
+        "training_backward": training,
         "kernel_source_digest": kernel_source_digest(),
     }
     del x, w, g, out, grads, env

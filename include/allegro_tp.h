@@ -63,6 +63,7 @@
 #ifndef ALLEGRO_TP_H
 #define ALLEGRO_TP_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -130,6 +131,29 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
                         const float *grad_out, const float *w, const float *Y,
                         float *grad_x, float *grad_env, float *grad_w, float *grad_Y,
                         void *stream);
+
+/* Bytes of device workspace that allegro_tp_backward_train needs for N centers:
+ * (N + 128) * n_paths * U floats.  Host-only; no GPU needed. */
+int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t *bytes);
+
+/* Training backward: everything allegro_tp_backward computes, plus the
+ * gradient of the path weights (needed to train them; the paper leaves the
+ * training kernels to future work, §II.D):
+ *   grad_path_w[p][u] = sum_e sum_{(i,j,k) in p} C_ijk x[e,u,i] env[c(e),u,j] grad_out[e,u,k]
+ * (for one scalar weight per path, sum grad_path_w over u).  The sum is
+ * deterministic: each center's edges are summed in order by the backward
+ * launch into workspace rows [N][n_paths][U], which two reduction launches then
+ * sum in a fixed order.  workspace is caller-owned device memory of at least
+ * allegro_tp_backward_workspace() bytes, 16-byte aligned, overwritten (no
+ * clearing needed); calls that share a workspace must not overlap.  N == 0
+ * sets grad_path_w to zero.  Errors as for allegro_tp_backward, plus
+ * ALLEGRO_E_INVALID for a missing or too small workspace. */
+int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
+                              const float *x, const float *env, const float *path_w,
+                              const float *grad_out, const float *w, const float *Y,
+                              float *grad_x, float *grad_env, float *grad_w, float *grad_Y,
+                              float *grad_path_w, void *workspace, size_t workspace_bytes,
+                              void *stream);
 
 /* Real spherical harmonics of the edge vectors, the embedding input of the
  * environment sum (Appendix "Mixed-Precision Architecture": embedded in fp64,

@@ -22,6 +22,8 @@ from .binding import (  # noqa: F401
     allegro_sh_backward,
     allegro_sh_forward,
     allegro_tp_backward,
+    allegro_tp_backward_train,
+    allegro_tp_backward_workspace,
     allegro_tp_forward,
     allegro_tp_plan_create,
     allegro_tp_plan_destroy,

@@ -27,7 +27,8 @@ ALLEGRO_VALIDATE = 4
 
 EXPORTED = (
     "allegro_tp_plan_create", "allegro_tp_plan_destroy", "allegro_tp_plan_query", "allegro_tp_plan_cg",
-    "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_sh_forward", "allegro_sh_backward",
+    "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_tp_backward_workspace",
+    "allegro_tp_backward_train", "allegro_sh_forward", "allegro_sh_backward",
     "allegro_last_error",
 )
 
@@ -57,6 +58,8 @@ def _load() -> ctypes.CDLL:
     lib.allegro_env_embed.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp]
     lib.allegro_tp_forward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp]
     lib.allegro_tp_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.allegro_tp_backward_workspace.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_size_t)]
+    lib.allegro_tp_backward_train.argtypes = [vp, i64, i64] + [vp] * 13 + [ctypes.c_size_t, vp]
     lib.allegro_sh_forward.argtypes = [vp, i64, vp, vp, vp]
     lib.allegro_sh_backward.argtypes = [vp, i64, vp, vp, vp, vp]
     lib.allegro_last_error.restype = ctypes.c_char_p
@@ -217,6 +220,47 @@ def allegro_tp_backward(plan: Plan, row_ptr, x, env, path_w, grad_out, w, Y, out
                                     _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw), _ptr(gy),
                                     _stream(stream, dev)))
     return gx, genv, gw, gy
+
+
+def allegro_tp_backward_workspace(plan: Plan, n_centers: int) -> int:
+    """Bytes of device workspace allegro_tp_backward_train needs for n_centers."""
+    out = ctypes.c_size_t()
+    _check(_lib.allegro_tp_backward_workspace(plan.handle, int(n_centers), ctypes.byref(out)))
+    return out.value
+
+
+def allegro_tp_backward_train(plan: Plan, row_ptr, x, env, path_w, grad_out, w, Y, outs=None, workspace=None,
+                              stream=None):
+    """Returns (grad_x, grad_env, grad_w, grad_Y, grad_path_w); workspace is a uint8 device tensor or None."""
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, x.shape[0])
+    _need(x, "x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(env, "env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(path_w, "path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    _need(grad_out, "grad_out", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(w, "w", (e, plan.U), torch.float32, dev)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    if outs is None:
+        outs = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(Y),
+                torch.empty_like(path_w))
+    gx, genv, gw, gy, gpw = outs
+    _need(gx, "grad_x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(genv, "grad_env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(gw, "grad_w", (e, plan.U), torch.float32, dev)
+    _need(gy, "grad_Y", (e, plan.d2), torch.float32, dev)
+    _need(gpw, "grad_path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    need = allegro_tp_backward_workspace(plan, n)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    if workspace.device != torch.device(dev) or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor on the same device")
+    _check(_lib.allegro_tp_backward_train(plan.handle, n, e, _ptr(row_ptr), _ptr(x), _ptr(env), _ptr(path_w),
+                                          _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw),
+                                          _ptr(gy), _ptr(gpw), _ptr(workspace),
+                                          workspace.numel() * workspace.element_size(), _stream(stream, dev)))
+    return gx, genv, gw, gy, gpw
 
 
 def allegro_sh_forward(plan: Plan, vec, Y=None, stream=None):

@@ -56,7 +56,7 @@ def _check_resources(report: str) -> str:
     for name, kv in sorted(rows.items()):
         if kv.get("ScratchSize", "0") != "0" or kv.get("VGPRs Spill", "0") != "0":
             bad.append(name)
-        out.append(f"{name} VGPRs={kv.get('VGPRs')} SGPRs={kv.get('TotalSGPRs')} "
+        out.append(f"{name} VGPRs={kv.get('VGPRs')} AGPRs={kv.get('AGPRs')} SGPRs={kv.get('TotalSGPRs')} "
                    f"scratch={kv.get('ScratchSize')} occupancy={kv.get('Occupancy')} lds={kv.get('LDS Size')}")
     if not rows:
         raise RuntimeError("no kernel resource report from hipcc")

@@ -305,6 +305,8 @@ struct KernelTraits {
   // waves per SIMD the register allocation must allow
   static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
   static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
+  // the path-weight accumulators add NP live registers per lane
+  static constexpr int bwd_occupancy(bool wg) { return wg ? (Core::LMAX >= 3 ? 1 : 2) : kBwdOccupancy; }
 };
 
 // ------------------------------------------------------ tensor product fwd
@@ -356,13 +358,13 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
 
 // ------------------------------------------------------ tensor product bwd
 // Pass 1 over channel half t: grad_x rows in place in the x tile, this lane's
-// grad_env partial sums in ge.
-template <class Core, int U, int T, int TF4>
+// grad_env partial sums in ge and, with WG, its path-weight gradient sums in sw.
+template <class Core, int U, int T, int TF4, bool WG>
 __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const float *__restrict__ g,
                                           const float *__restrict__ env, const float *__restrict__ path_w,
                                           float *__restrict__ grad_x, float4 *tile_x, float4 *tile_g, int64_t n,
                                           int64_t e0, int64_t e1, int64_t n_slabs, int t, int lane,
-                                          float (&ge)[Core::D2]) {
+                                          float (&ge)[Core::D2], float (&sw)[Core::NP]) {
   constexpr int D1 = Core::D1, D2 = Core::D2;
   const int u = lane % Lanes<U>::LPE + t * kWave;
   RegWeights<Core::NP> wr;
@@ -383,7 +385,9 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
       if (row_valid<U>(e0, e1, s0 + s, lane)) {
         // x row in, grad_x row out, in place in the LDS tile
         float *row = tx + (s * kWave + lane) * D1;
-        Core::bwd(row, er, wr, tg + (s * kWave + lane) * D1, row, ge);
+        const float *grow = tg + (s * kWave + lane) * D1;
+        if constexpr (WG) Core::wgrad(row, er, grow, sw);
+        Core::bwd(row, er, wr, grow, row, ge);
       }
     }
     lds_sync<1>();
@@ -392,12 +396,14 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
   }
 }
 
-template <class Core, int U>
-__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kBwdOccupancy))) void tp_backward_kernel(
+// With WG the kernel also writes center n's path-weight gradient, summed over
+// its edges, to pw_part[n][p][u] (the first of the two reduction stages).
+template <class Core, int U, bool WG>
+__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::bwd_occupancy(WG)))) void tp_backward_kernel(
         const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
         const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
         const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
-        float *__restrict__ grad_w, float *__restrict__ grad_Y) {
+        float *__restrict__ grad_w, float *__restrict__ grad_Y, float *__restrict__ pw_part) {
   using L = Lanes<U>;
   constexpr int D1 = Core::D1, D2 = Core::D2;
   constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
@@ -425,8 +431,27 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
     const int u = ul + t * kWave;
-    float ge[D2];
-    bwd_pass1<Core, U, T, TILE_F4>(x, g, env, path_w, grad_x, tile_x, tile_g, n, e0, e1, n_slabs, t, lane, ge);
+    float ge[D2], sw[Core::NP];
+    if constexpr (WG) {
+#pragma unroll
+      for (int p = 0; p < Core::NP; ++p) sw[p] = 0.0f;
+    }
+    bwd_pass1<Core, U, T, TILE_F4, WG>(x, g, env, path_w, grad_x, tile_x, tile_g, n, e0, e1, n_slabs, t, lane, ge,
+                                       sw);
+    if constexpr (WG) {
+      // lane groups hold the same channel: butterfly sums in a fixed order (the
+      // two operands of each step are swapped between partner lanes, so every
+      // lane of a channel ends with the same bits)
+#pragma unroll
+      for (int p = 0; p < Core::NP; ++p) {
+#pragma unroll
+        for (int off = L::LPE; off < kWave; off *= 2) sw[p] += __shfl_xor(sw[p], off);
+      }
+      if (grp == 0) {
+#pragma unroll
+        for (int p = 0; p < Core::NP; ++p) pw_part[(n * Core::NP + p) * U + u] = sw[p];
+      }
+    }
     // grad_env of this channel half goes straight to its output
     if constexpr (L::G == 1) {
       store_row<D2>(grad_env + (n * U + u) * D2, ge);
@@ -618,6 +643,45 @@ __global__ void csr_check_kernel(int64_t N, int64_t E, const int64_t *__restrict
   }
 }
 
+// ------------------------------------------- path-weight gradient reduction
+// Stages two and three of grad_path_w: column c = p * U + u of pw_part[N][P*U]
+// is summed over the centers, first within kPwChunks fixed ranges of rows, then
+// over the ranges, each sum in a fixed order (run-to-run bit-identical).
+constexpr int kPwChunks = 128;
+
+__global__ __launch_bounds__(256) void pw_reduce_rows_kernel(int64_t N, int cols, const float *__restrict__ part,
+                                                             float *__restrict__ chunk_sums) {
+  const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (c >= cols) return;
+  const int64_t per = (N + kPwChunks - 1) / kPwChunks;
+  const int64_t r0 = int64_t(blockIdx.y) * per;
+  const int64_t r1 = r0 + per < N ? r0 + per : N;
+  float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+  int64_t r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    a0 += part[r * cols + c];
+    a1 += part[(r + 1) * cols + c];
+    a2 += part[(r + 2) * cols + c];
+    a3 += part[(r + 3) * cols + c];
+  }
+  for (; r < r1; ++r) a0 += part[r * cols + c];
+  chunk_sums[int64_t(blockIdx.y) * cols + c] = (a0 + a1) + (a2 + a3);
+}
+
+__global__ __launch_bounds__(256) void pw_reduce_chunks_kernel(int cols, const float *__restrict__ chunk_sums,
+                                                               float *__restrict__ grad_pw) {
+  const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (c >= cols) return;
+  float a = 0.0f;
+  for (int r = 0; r < kPwChunks; ++r) a += chunk_sums[r * cols + c];
+  grad_pw[c] = a;
+}
+
+__global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restrict__ p) {
+  const int i = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (i < n) p[i] = 0.0f;
+}
+
 // ------------------------------------------------------------- host side
 thread_local std::string g_last_error;
 
@@ -647,7 +711,7 @@ namespace {
 using EnvFn = void (*)(dim3, hipStream_t, int64_t, const int64_t *, const float *, const float *, float *);
 using FwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, float *);
 using BwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, const float *,
-                       const float *, const float *, float *, float *, float *, float *);
+                       const float *, const float *, float *, float *, float *, float *, float *);
 
 template <int U, int D2, bool DET>
 void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const float *w, const float *Y, float *env) {
@@ -660,17 +724,19 @@ void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, con
   hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave), 0, s, rp, x, env, pw, out);
 }
 
-template <class Core, int U>
+template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
-                const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy) {
-  hipLaunchKernelGGL((tp_backward_kernel<Core, U>), grid, dim3(kWave), 0, s, rp, x, env, pw, g, w, Y, gx, genv, gw,
-                     gy);
+                const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
+                float *pw_part) {
+  hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave), 0, s, rp, x, env, pw, g, w, Y, gx, genv,
+                     gw, gy, pw_part);
 }
 
 struct Kernels {
   EnvFn env = nullptr;
   FwdFn fwd = nullptr;
   BwdFn bwd = nullptr;
+  BwdFn bwd_wg = nullptr;  // also writes the per-center path-weight gradient
 };
 
 template <int LMAX, bool FULL, int U>
@@ -679,7 +745,8 @@ Kernels kernels_for(bool det) {
   Kernels k;
   k.env = det ? &launch_env<U, Core::D2, true> : &launch_env<U, Core::D2, false>;
   k.fwd = &launch_fwd<Core, U>;
-  k.bwd = &launch_bwd<Core, U>;
+  k.bwd = &launch_bwd<Core, U, false>;
+  k.bwd_wg = &launch_bwd<Core, U, true>;
   return k;
 }
 
@@ -870,8 +937,57 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
   if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
   const Kernels k = select(plan);
   if (!k.bwd) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
-  k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y);
+  k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, nullptr);
   return after_launch("allegro_tp_backward");
+}
+
+int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t *bytes) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (N < 0 || N >= (int64_t(1) << 31)) return fail(ALLEGRO_E_INVALID, "N=%lld out of range", (long long)N);
+  if (!bytes) return fail(ALLEGRO_E_INVALID, "bytes is NULL");
+  const int64_t cols = int64_t(plan->table.paths.size()) * plan->U;
+  *bytes = size_t((N + kPwChunks) * cols) * sizeof(float);
+  return ALLEGRO_OK;
+}
+
+int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
+                              const float *x, const float *env, const float *path_w, const float *grad_out,
+                              const float *w, const float *Y, float *grad_x, float *grad_env, float *grad_w,
+                              float *grad_Y, float *grad_path_w, void *workspace, size_t workspace_bytes,
+                              void *stream) {
+  int rc = check_sizes(plan, N, E, row_ptr);
+  if (rc) return rc;
+  if ((rc = check_tensor(grad_path_w, "grad_path_w"))) return rc;
+  const int cols = int(plan->table.paths.size()) * plan->U;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (N == 0) {  // no centers, no edges: the gradient is zero
+    hipLaunchKernelGGL(zero_floats_kernel, dim3(unsigned((cols + 255) / 256)), dim3(256), 0, s, cols, grad_path_w);
+    return after_launch("allegro_tp_backward_train");
+  }
+  size_t need = 0;
+  (void)allegro_tp_backward_workspace(plan, N, &need);
+  if ((rc = check_tensor(workspace, "workspace"))) return rc;
+  if (workspace_bytes < need)
+    return fail(ALLEGRO_E_INVALID, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes, need);
+  if ((rc = check_tensor(grad_env, "grad_env")) || (rc = check_tensor(env, "env")) ||
+      (rc = check_tensor(path_w, "path_w")))
+    return rc;
+  if (E > 0 && ((rc = check_tensor(x, "x")) || (rc = check_tensor(grad_out, "grad_out")) ||
+                (rc = check_tensor(w, "w")) || (rc = check_tensor(Y, "Y")) || (rc = check_tensor(grad_x, "grad_x")) ||
+                (rc = check_tensor(grad_w, "grad_w")) || (rc = check_tensor(grad_Y, "grad_Y"))))
+    return rc;
+  auto *mp = const_cast<allegro_tp_plan *>(plan);
+  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const Kernels k = select(plan);
+  if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  float *part = static_cast<float *>(workspace);
+  float *chunks = part + N * cols;
+  k.bwd_wg(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, part);
+  if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
+  const unsigned cb = unsigned((cols + 255) / 256);
+  hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
+  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, cols, chunks, grad_path_w);
+  return after_launch("allegro_tp_backward_train");
 }
 
 // One edge per thread in 256-thread blocks; the grid's x extent stays below 2^31.

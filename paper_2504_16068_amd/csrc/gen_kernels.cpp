@@ -10,8 +10,11 @@
 //   bwd: Q_ij    = sum_{p with blocks (a,b)} sum_k C (W(p) g[k])
 //        gx[i]   = sum_j Q_ij env[j]           (overwritten; may alias x)
 //        ge[j]  += sum_i Q_ij x[i]             (accumulated across edges)
-// which is the tensor product and its VJP with respect to x and env, written
-// per pair of input blocks so that at most one block of temporaries is live.
+//   wgrad: acc[p] += sum_k g[k] sum_{(i,j,k) in p} C q_ij
+//        (the path-weight gradient of one edge and channel, accumulated)
+// which is the tensor product and its VJP with respect to x, env and the path
+// weights, written per pair of input blocks so that at most one block of
+// temporaries is live.
 // W is any accessor with W(p) = the lane's weight of path p.
 //
 // Usage: gen_kernels <output.inc>
@@ -107,6 +110,34 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   }
   for (int k = 0; k < t.d1; ++k)
     if (!out_init[k]) std::fprintf(f, "    out[%d] = 0.0f;\n", k);
+  std::fprintf(f, "  }\n");
+
+  // ------------------------------------------------- path-weight gradient
+  std::fprintf(f,
+               "  static __device__ __forceinline__ void wgrad(const float *__restrict__ x, const float *__restrict__ env,\n"
+               "                                               const float *__restrict__ g, float (&acc)[NP]) {\n");
+  for (const Group &g : groups) {
+    std::fprintf(f, "    { // x block %d with env block %d\n", g.a, g.b);
+    std::set<std::pair<int, int>> pairs;
+    for (int p : g.paths)
+      for (const auto &e : per_path[p]) pairs.insert({e.i, e.j});
+    for (const auto &ij : pairs)
+      std::fprintf(f, "      const float q%d_%d = x[%d] * env[%d];\n", ij.first, ij.second, ij.first, ij.second);
+    for (int p : g.paths) {
+      std::map<int, std::vector<allegro::CGEntry>> by_k;
+      for (const auto &e : per_path[p]) by_k[e.k].push_back(e);
+      for (const auto &kv : by_k) {
+        std::fprintf(f, "      { float s;");
+        bool first = true;
+        for (const auto &e : kv.second) {
+          std::fprintf(f, " %s", accumulate("s", first, e.value, "q" + std::to_string(e.i) + "_" + std::to_string(e.j)).c_str());
+          first = false;
+        }
+        std::fprintf(f, " acc[%d] = __builtin_fmaf(g[%d], s, acc[%d]); }\n", p, kv.first, p);
+      }
+    }
+    std::fprintf(f, "    }\n");
+  }
   std::fprintf(f, "  }\n");
 
   // ---------------------------------------------------------------- backward

@@ -123,6 +123,16 @@ def test_entry_points_reject_bad_arguments_before_any_launch():
     rc, msg = _err(lib.allegro_sh_backward, h, 4, ok_ptr, ok_ptr, None, None)
     assert rc == binding.ALLEGRO_E_INVALID and "grad_vec is NULL" in msg
     assert lib.allegro_sh_forward(h, 0, None, None, None) == binding.ALLEGRO_OK
+    # training backward: workspace size is host arithmetic; missing / short workspace is rejected
+    assert binding.allegro_tp_backward_workspace(plan, 10) == (10 + 128) * plan.n_paths * 64 * 4
+    args = [h, 3, 5, ok_rp] + [ok_ptr] * 11
+    rc, msg = _err(lib.allegro_tp_backward_train, *args, None, 1 << 20, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "workspace is NULL" in msg
+    rc, msg = _err(lib.allegro_tp_backward_train, *args, ok_ptr, 100, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "smaller" in msg
+    args[14] = None
+    rc, msg = _err(lib.allegro_tp_backward_train, *args, ok_ptr, 1 << 20, None)
+    assert rc == binding.ALLEGRO_E_INVALID and "grad_path_w is NULL" in msg
     # empty problem: successful no-op
     for fn, nargs in ((lib.allegro_env_embed, 5), (lib.allegro_tp_forward, 6), (lib.allegro_tp_backward, 12)):
         rc = fn(h, 0, 0, *([None] * (nargs - 1)), None)

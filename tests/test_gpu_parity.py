@@ -293,3 +293,111 @@ def test_sh_headline_vectors_sampled(at):
     assert np.all(np.abs(yh[idx] - ref_y) <= 2.0 ** -23 * np.abs(ref_y) + 1e-12)
     ref_g = osh.sh_backward(2, vec[idx], gy.cpu().numpy()[idx])
     assert block_rel_err(gvh[idx], ref_g) <= 1e-7
+
+
+# ------------------------------------------ training backward (path weights)
+
+def _train(at, plan, rp, x, env, pw, g, w, y):
+    n = rp.numel() - 1
+    ws = torch.empty(at.allegro_tp_backward_workspace(plan, n), dtype=torch.uint8, device=DEV)
+    res = at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, workspace=ws)
+    torch.cuda.synchronize()
+    return res, ws
+
+
+def _same_bits(a, b):
+    return torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+@pytest.mark.parametrize("case", ["tiny", "small"] + [f"edge{i}" for i in range(len(EDGE_CASES))])
+def test_train_backward_parity(at, case):
+    if case.startswith("edge"):
+        lmax, full, U, degrees = EDGE_CASES[int(case[4:])]
+        data = _synthetic(lmax, full, U, degrees, seed=7 + lmax * 10 + U)
+    else:
+        graph = workloads.make_graph(case)
+        cfg = graph.config
+        lmax, full, U = cfg.lmax, cfg.full_parity, cfg.U
+        x, w, pw, g = workloads.host_features(cfg, graph.n_edges)
+        data = (graph.row_ptr, x, w, graph.Y, pw, g)
+    _note(f"[gpu] training backward {case}: lmax={lmax} full={full} U={U}")
+    plan = _plan(at, lmax, U, full)
+    rp, xd, wd, yd, pwd, gd = (_t(a) for a in data)
+    env = at.allegro_env_embed(plan, rp, wd, yd)
+    base = at.allegro_tp_backward(plan, rp, xd, env, pwd, gd, wd, yd)
+    (gx, genv, gw, gy, gpw), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
+    # the other gradients are those of the inference backward, bit for bit
+    for a, b in zip((gx, genv, gw, gy), base):
+        assert _same_bits(a, b)
+    t = otp.TensorProduct(lmax, full)
+    ref = t.path_weight_grad(data[0], data[1], otp.env_embed(data[0], data[2], data[3]), data[5])
+    err = block_rel_err(gpw.cpu().numpy(), ref)
+    _note(f"training backward {case}: grad_path_w err={err:.2e}")
+    assert err <= BWD_TOL
+    # deterministic: a second call gives the same bits
+    (_, _, _, _, gpw2), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
+    assert _same_bits(gpw, gpw2)
+
+
+def test_train_backward_without_edges(at):
+    _note("[gpu] training backward with E = 0 (N = 3) and N = 0")
+    plan = _plan(at, 2, 32, False)
+    pw = torch.ones((plan.n_paths, 32), device=DEV)
+    x = torch.empty((0, 32, plan.d1), device=DEV)
+    w, y = torch.empty((0, 32), device=DEV), torch.empty((0, plan.d2), device=DEV)
+    for n in (3, 0):
+        rp = torch.zeros(n + 1, dtype=torch.int64, device=DEV)
+        env = torch.randn((n, 32, plan.d2), device=DEV)
+        outs = (torch.empty_like(x), torch.full_like(env, 5.0), torch.empty_like(w), torch.empty_like(y),
+                torch.full_like(pw, 9.0))
+        (_, genv, _, _, gpw), _ = (at.allegro_tp_backward_train(plan, rp, x, env, pw, x, w, y, outs=outs), None)
+        torch.cuda.synchronize()
+        assert torch.count_nonzero(gpw).item() == 0 and torch.count_nonzero(genv).item() == 0
+
+
+def test_train_backward_rejects_small_workspace(at):
+    plan = _plan(at, 1, 16, False)
+    rp = torch.tensor([0, 2], dtype=torch.int64, device=DEV)
+    x = torch.zeros((2, 16, plan.d1), device=DEV)
+    w, y = torch.zeros((2, 16), device=DEV), torch.zeros((2, plan.d2), device=DEV)
+    env, pw = torch.zeros((1, 16, plan.d2), device=DEV), torch.zeros((plan.n_paths, 16), device=DEV)
+    ws = torch.empty(at.allegro_tp_backward_workspace(plan, 1) - 16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(at.AllegroError) as ex:
+        at.allegro_tp_backward_train(plan, rp, x, env, pw, x, w, y, workspace=ws)
+    assert ex.value.code == at.ALLEGRO_E_INVALID and "workspace" in str(ex.value)
+
+
+@pytest.mark.parametrize("name", ["headline", "high_order", "large"])
+def test_train_backward_full_size(at, name, n_samples=16):
+    """Per-center partial sums (the workspace's first N * P * U floats) on sampled
+    centers against the oracle; the reduction against the fp64 sum of all rows."""
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    _note(f"[gpu] training backward {name}: N={graph.n_atoms} E={graph.n_edges} (sampled)")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    x, w, g = workloads.device_features(cfg, graph.n_edges, DEV)
+    pw = workloads.path_weights(cfg)
+    rp, yd, pwd = _t(graph.row_ptr), _t(graph.Y), _t(pw)
+    env = at.allegro_env_embed(plan, rp, w, yd)
+    base_gx = at.allegro_tp_backward(plan, rp, x, env, pwd, g, w, yd)[0]
+    (gx, _, _, _, gpw), ws = _train(at, plan, rp, x, env, pwd, g, w, yd)
+    assert _same_bits(gx, base_gx)
+    del gx, base_gx
+    n, cols = graph.n_atoms, plan.n_paths * cfg.U
+    part = ws[: n * cols * 4].view(torch.float32).view(n, plan.n_paths, cfg.U)
+    rng = np.random.default_rng(cfg.index + 50)
+    centers = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, n_samples)]))
+    t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
+    for c in centers:
+        s, e = int(graph.row_ptr[c]), int(graph.row_ptr[c + 1])
+        xs, ws_, gs = x[s:e].cpu().numpy(), w[s:e].cpu().numpy(), g[s:e].cpu().numpy()
+        local = np.array([0, e - s], np.int64)
+        ref = t.path_weight_grad(local, xs, otp.env_embed(local, ws_, graph.Y[s:e]), gs)
+        assert block_rel_err(part[c].cpu().numpy(), ref) <= BWD_TOL, c
+    ph = part.cpu().numpy().astype(np.float64).reshape(n, cols)
+    total = ph.sum(axis=0)
+    # recursive-summation bound: at most ceil(ceil(N / 128) / 4) + 130 sequential fp32 additions
+    depth = -(-(-(-n // 128)) // 4) + 130
+    bound = 1.01 * depth * 2.0 ** -24 * np.abs(ph).sum(axis=0)
+    got = gpw.cpu().numpy().reshape(cols).astype(np.float64)
+    assert np.all(np.abs(got - total) <= bound)
