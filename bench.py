@@ -24,6 +24,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import re
 import os
 import sys
 import time
@@ -97,7 +98,9 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
     copy_kib = (4 << 30) / 1024
 
     def per_launch(rows, kernel):
-        vals = [float(r["Counter_Value"]) for r in rows if kernel in r["Kernel_Name"]]
+        # the inference backward only (template flag false), not the training variant
+        pat = re.compile(kernel + r"<.*,\s*false>")
+        vals = [float(r["Counter_Value"]) for r in rows if pat.search(r["Kernel_Name"])]
         return sum(vals) / len(vals), len(vals)
 
     fr, wr = read(fetch_csv), read(write_csv)
