@@ -27,6 +27,7 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "allegro_tp.h"
@@ -300,13 +301,30 @@ struct RegWeights {
   __device__ __forceinline__ float operator()(int p) const { return r[p]; }
 };
 
+// Path weights read at use from the lane's column of path_w (an L1/L2 hit after
+// the first edge) instead of NP registers; renew() hides the pointer from
+// loop-invariant code motion so the loads are not hoisted back into registers.
+struct CachedWeights {
+  typedef const __attribute__((address_space(1))) float *gptr;
+  gptr col;
+  int U;
+  __device__ __forceinline__ void load(const float *__restrict__ path_w, int U_, int u) {
+    col = (gptr)(path_w + u);
+    U = U_;
+  }
+  __device__ __forceinline__ void renew() { asm volatile("" : "+v"(col)); }
+  __device__ __forceinline__ float operator()(int p) const { return col[p * U]; }
+};
+
 template <class Core>
 struct KernelTraits {
   // waves per SIMD the register allocation must allow
   static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
   static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
-  // the path-weight accumulators add NP live registers per lane
-  static constexpr int bwd_occupancy(bool wg) { return wg ? (Core::LMAX >= 3 ? 1 : 2) : kBwdOccupancy; }
+  // the path-weight accumulators add NP live registers per lane; at lmax 3 the
+  // training variant makes room for them by reading the weights from cache
+  static constexpr bool cached_weights(bool wg) { return wg && Core::LMAX >= 3; }
+  static constexpr int bwd_occupancy(bool wg) { return wg ? 2 : kBwdOccupancy; }
 };
 
 // ------------------------------------------------------ tensor product fwd
@@ -367,7 +385,8 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
                                           float (&ge)[Core::D2], float (&sw)[Core::NP]) {
   constexpr int D1 = Core::D1, D2 = Core::D2;
   const int u = lane % Lanes<U>::LPE + t * kWave;
-  RegWeights<Core::NP> wr;
+  constexpr bool kCached = KernelTraits<Core>::cached_weights(WG);
+  typename std::conditional<kCached, CachedWeights, RegWeights<Core::NP>>::type wr;
   wr.load(path_w, U, u);
   float er[D2];
   load_row<D2>(env + (n * U + u) * D2, er);
@@ -386,6 +405,7 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
         // x row in, grad_x row out, in place in the LDS tile
         float *row = tx + (s * kWave + lane) * D1;
         const float *grow = tg + (s * kWave + lane) * D1;
+        if constexpr (kCached) wr.renew();
         if constexpr (WG) Core::wgrad(row, er, grow, sw);
         Core::bwd(row, er, wr, grow, row, ge);
       }
