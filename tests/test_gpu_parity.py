@@ -73,9 +73,17 @@ def _compare(t, gpu, ref, tag):
         "grad_w": (block_rel_err(gw, rgw), BWD_TOL),
         "grad_Y": (block_rel_err(gy, rgy, t.env_slices), BWD_TOL),
     }
-    _note(f"{tag}: " + ", ".join(f"{k}={v:.2e}" for k, (v, _) in errs.items()))
+    plain = {k: _max_rel(g, o) for k, g, o in (("env", env, renv), ("out", out, rout), ("grad_x", gx, rgx),
+                                                ("grad_env", genv, rgenv), ("grad_w", gw, rgw), ("grad_Y", gy, rgy))}
+    _note(f"{tag}: " + ", ".join(f"{k}={v:.2e}" for k, (v, _) in errs.items())
+          + " | max|g-o|/max|o|: " + ", ".join(f"{k}={v:.2e}" for k, v in plain.items()))
     bad = {k: v for k, (v, tol) in errs.items() if not v <= tol}
     assert not bad, f"{tag}: parity failed {bad}"
+
+
+def _max_rel(got, ref):
+    got, ref = np.asarray(got, np.float64), np.asarray(ref, np.float64)
+    return float(np.max(np.abs(got - ref)) / max(np.max(np.abs(ref)), 1e-300)) if ref.size else 0.0
 
 
 def _np(gpu):
@@ -401,3 +409,42 @@ def test_train_backward_full_size(at, name, n_samples=16):
     bound = 1.01 * depth * 2.0 ** -24 * np.abs(ph).sum(axis=0)
     got = gpw.cpu().numpy().reshape(cols).astype(np.float64)
     assert np.all(np.abs(got - total) <= bound)
+
+
+def test_scalar_path_weights_broadcast(at):
+    """One scalar weight per path, passed broadcast over the channels; its gradient is grad_path_w summed over u."""
+    graph = workloads.make_graph("small")
+    cfg = graph.config
+    x, w, _, g = workloads.host_features(cfg, graph.n_edges)
+    _note("[gpu] scalar path weights broadcast over channels, small")
+    scal = np.random.default_rng(31).standard_normal((workloads.dims(cfg.lmax, cfg.full_parity)[2], 1))
+    pw = np.ascontiguousarray(np.broadcast_to(scal, (scal.shape[0], cfg.U))).astype(np.float32)
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    rp, xd, wd, yd, pwd, gd = (_t(a) for a in (graph.row_ptr, x, w, graph.Y, pw, g))
+    env = at.allegro_env_embed(plan, rp, wd, yd)
+    out = at.allegro_tp_forward(plan, rp, xd, env, pwd)
+    (_, _, _, _, gpw), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
+    t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
+    renv = otp.env_embed(graph.row_ptr, w, graph.Y)
+    assert block_rel_err(out.cpu().numpy(), t.forward(graph.row_ptr, x, renv, pw), t.x_slices) <= FWD_TOL
+    ref_scalar = t.path_weight_grad(graph.row_ptr, x, renv, g).sum(axis=1)
+    got_scalar = gpw.cpu().numpy().astype(np.float64).sum(axis=1)
+    assert block_rel_err(got_scalar, ref_scalar) <= BWD_TOL
+
+
+@pytest.mark.parametrize("name", ["headline", "high_order"])
+def test_deterministic_env_full_size_sampled(at, name, n_samples=32):
+    """Deterministic env at full size: sampled centers bit-equal to the fp32 sequential replay."""
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    _note(f"[gpu] deterministic env {name} (sampled)")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity, det=True)
+    _, w, _ = workloads.device_features(cfg, graph.n_edges, DEV)
+    env = at.allegro_env_embed(plan, _t(graph.row_ptr), w, _t(graph.Y))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(cfg.index + 70)
+    centers = np.unique(np.concatenate([[0, graph.n_atoms - 1], rng.integers(0, graph.n_atoms, n_samples)]))
+    for c in centers:
+        s, e = int(graph.row_ptr[c]), int(graph.row_ptr[c + 1])
+        ref = otp.env_embed_fp32_replay(np.array([0, e - s], np.int64), w[s:e].cpu().numpy(), graph.Y[s:e])
+        assert np.array_equal(env[c:c + 1].cpu().numpy().view(np.uint32), ref.view(np.uint32)), c
