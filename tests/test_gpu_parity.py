@@ -448,3 +448,52 @@ def test_deterministic_env_full_size_sampled(at, name, n_samples=32):
         s, e = int(graph.row_ptr[c]), int(graph.row_ptr[c + 1])
         ref = otp.env_embed_fp32_replay(np.array([0, e - s], np.int64), w[s:e].cpu().numpy(), graph.Y[s:e])
         assert np.array_equal(env[c:c + 1].cpu().numpy().view(np.uint32), ref.view(np.uint32)), c
+
+
+def test_step_replays_in_a_hip_graph(at):
+    """The whole step (harmonics, embedding, forward, training backward, harmonics VJP)
+    captured once into a HIP graph and replayed several times, with eager work and
+    synchronisation in between; every replay must equal the eager result bit for bit."""
+    graph = workloads.make_graph("small")
+    cfg = graph.config
+    x, w, pw, g = workloads.host_features(cfg, graph.n_edges)
+    _note("[gpu] HIP graph replay of the step, small")
+    plan = _plan(at, cfg.lmax, cfg.U, cfg.full_parity)
+    rp, xd, wd, pwd, gd, vec = (_t(a) for a in (graph.row_ptr, x, w, pw, g, graph.vec))
+    n, e = graph.n_atoms, graph.n_edges
+    y = torch.empty((e, plan.d2), device=DEV)
+    env = torch.empty((n, cfg.U, plan.d2), device=DEV)
+    out = torch.empty_like(xd)
+    outs = (torch.empty_like(xd), torch.empty_like(env), torch.empty_like(wd), torch.empty_like(y),
+            torch.empty_like(pwd))
+    gvec = torch.empty((e, 3), device=DEV, dtype=torch.float64)
+    ws = torch.empty(at.allegro_tp_backward_workspace(plan, n), dtype=torch.uint8, device=DEV)
+
+    def step():
+        at.allegro_sh_forward(plan, vec, Y=y)
+        at.allegro_env_embed(plan, rp, wd, y, env=env)
+        at.allegro_tp_forward(plan, rp, xd, env, pwd, out=out)
+        at.allegro_tp_backward_train(plan, rp, xd, env, pwd, gd, wd, y, outs=outs, workspace=ws)
+        at.allegro_sh_backward(plan, vec, outs[3], grad_vec=gvec)
+
+    results = (y, env, out, *outs, gvec)
+    step()
+    torch.cuda.synchronize()
+    eager = [r.clone() for r in results]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    hip_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(hip_graph):
+        step()
+    for rep in range(3):
+        for r in results:
+            r.fill_(float("nan"))  # eager work between replays
+        torch.cuda.synchronize()
+        hip_graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(results, eager):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), rep
