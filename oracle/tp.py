@@ -28,9 +28,9 @@ Precision (Appendix, "Mixed-Precision Architecture"): the GPU computes in fp32;
 the oracle evaluates the definition in fp64 on the same fp32 input values.
 
 Two forms: ``*_loops`` are plain nested Python loops (tiny inputs, brute force);
-the default forms take the same steps per path with numpy einsum over the dense
-coupling blocks, processed in chunks of edges.  Both must agree to fp64
-rounding.
+the default forms take the same steps per path over the dense coupling blocks,
+in chunks of edges: the outer product of the two input blocks, flattened, times
+the flattened block (a matmul).  Both must agree to fp64 rounding.
 """
 
 from __future__ import annotations
@@ -55,6 +55,17 @@ def _f64(a) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- env
+
+def _outer(xa, eb) -> np.ndarray:
+    """[e * u, i * j] products x_i env_j (rows (e, u), columns i major)."""
+    n = xa.shape[0] * xa.shape[1]
+    return (xa[:, :, :, None] * eb[:, :, None, :]).reshape(n, -1)
+
+
+def _flat(blk) -> np.ndarray:
+    """Coupling block C[i, j, k] as a [(i, j), k] matrix, i major."""
+    return blk.reshape(-1, blk.shape[2])
+
 
 def env_embed(row_ptr, w, Y) -> np.ndarray:
     """env[n, u, j] = sum over the segment of n of w[e, u] Y[e, j], fp64."""
@@ -129,6 +140,13 @@ class TensorProduct:
         self.x_slices = [slice(o, o + 2 * l + 1) for o, (l, _) in zip(xo, self.x_irreps)]
         self.env_slices = [slice(o, o + 2 * l + 1) for o, (l, _) in zip(eo, self.env_irreps)]
 
+    def _groups(self):
+        """Paths grouped by their input blocks (a, b), which share the products x_i env_j."""
+        groups = {}
+        for p, (a, b, _) in enumerate(self.paths):
+            groups.setdefault((a, b), []).append(p)
+        return groups.items()
+
     @property
     def n_paths(self) -> int:
         return len(self.paths)
@@ -146,11 +164,12 @@ class TensorProduct:
         for s in range(0, n_edges, _CHUNK):
             t = min(s + _CHUNK, n_edges)
             xe, ee = x64[s:t], env64[c[s:t]]
-            for p, (a, b, cc) in enumerate(self.paths):
-                blk = self.blocks[p]
-                contrib = np.einsum("eui,euj,ijk->euk", xe[:, :, self.x_slices[a]],
-                                    ee[:, :, self.env_slices[b]], blk, optimize=True)
-                out[s:t, :, self.x_slices[cc]] += w64[p][None, :, None] * contrib
+            for (a, b), group in self._groups():
+                q = _outer(xe[:, :, self.x_slices[a]], ee[:, :, self.env_slices[b]])
+                for p in group:
+                    cc = self.paths[p][2]
+                    contrib = (q @ _flat(self.blocks[p])).reshape(t - s, n_ch, -1)
+                    out[s:t, :, self.x_slices[cc]] += w64[p][None, :, None] * contrib
         return out
 
     def forward_loops(self, row_ptr, x, env, W) -> np.ndarray:
@@ -188,9 +207,10 @@ class TensorProduct:
                 blk = self.blocks[p]
                 wp = w64[p][None, :, None]
                 xa, eb, gc = xe[:, :, self.x_slices[a]], ee[:, :, self.env_slices[b]], ge[:, :, self.x_slices[cc]]
-                grad_x[s:t, :, self.x_slices[a]] += wp * np.einsum("euj,euk,ijk->eui", eb, gc, blk, optimize=True)
-                grad_env_edge[s:t, :, self.env_slices[b]] += wp * np.einsum("eui,euk,ijk->euj", xa, gc, blk,
-                                                                            optimize=True)
+                # r[e, u, i, j] = sum_k C_ijk g[e, u, k]
+                r = (gc.reshape(-1, gc.shape[2]) @ _flat(blk).T).reshape(gc.shape[:2] + blk.shape[:2])
+                grad_x[s:t, :, self.x_slices[a]] += wp * np.sum(r * eb[:, :, None, :], axis=3)
+                grad_env_edge[s:t, :, self.env_slices[b]] += wp * np.sum(r * xa[:, :, :, None], axis=2)
         grad_env = np.zeros_like(env64)
         np.add.at(grad_env, c, grad_env_edge)
         grad_w, grad_y = env_embed_backward(row_ptr, grad_env, w, Y)
@@ -237,9 +257,12 @@ class TensorProduct:
         for s in range(0, n_edges, _CHUNK):
             t = min(s + _CHUNK, n_edges)
             xe, ee, ge = x64[s:t], env64[c[s:t]], g64[s:t]
-            for p, (a, b, cc) in enumerate(self.paths):
-                grad[p] += np.einsum("eui,euj,euk,ijk->u", xe[:, :, self.x_slices[a]], ee[:, :, self.env_slices[b]],
-                                     ge[:, :, self.x_slices[cc]], self.blocks[p], optimize=True)
+            for (a, b), group in self._groups():
+                q = _outer(xe[:, :, self.x_slices[a]], ee[:, :, self.env_slices[b]])
+                for p in group:
+                    cc = self.paths[p][2]
+                    contrib = (q @ _flat(self.blocks[p])).reshape(t - s, n_ch, -1)
+                    grad[p] += np.sum(contrib * ge[:, :, self.x_slices[cc]], axis=(0, 2))
         return grad
 
     def path_weight_grad_loops(self, row_ptr, x, env, g) -> np.ndarray:

@@ -68,6 +68,11 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   std::fprintf(f, "template <> struct TPCore<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
   std::fprintf(f, "  static constexpr int LMAX = %d, D1 = %d, D2 = %d, NP = %d, NNZ = %d;\n", t.lmax, t.d1, t.d2, np,
                int(t.entries.size()));
+  // x irrep of each component (the per-irrep channel mixing acts block by block)
+  std::fprintf(f, "  static constexpr int NX = %d;\n  static constexpr int XIRREP[%d] = {", int(t.x_irreps.size()), t.d1);
+  for (int a = 0, k = 0; a < int(t.x_irreps.size()); ++a)
+    for (int m = 0; m < 2 * t.x_irreps[a].l + 1; ++m, ++k) std::fprintf(f, "%s%d", k ? ", " : "", a);
+  std::fprintf(f, "};\n");
 
   // entries grouped per path
   std::vector<std::vector<allegro::CGEntry>> per_path(np);

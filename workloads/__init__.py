@@ -47,6 +47,10 @@ CONFIGS = {
     "headline": Config("headline", 2, 20000, _box(20000), 5.0, 64, 2, True, False),
     "large": Config("large", 3, 100000, _box(100000), 6.0, 64, 2, True, False),
     "high_order": Config("high_order", 4, 20000, _box(20000), 5.0, 128, 3, True, False),
+    # one Allegro layer at the medium model shape of Table I (lmax 3, 64 features),
+    # latent width L and MLP hidden width H as stated (readings)
+    "layer_small": Config("layer_small", 5, 100, _box(100), 4.5, 64, 3, True, True, {"L": 64, "H": 128}),
+    "medium_layer": Config("medium_layer", 6, 20000, _box(20000), 5.0, 64, 3, True, False, {"L": 64, "H": 128}),
 }
 
 
@@ -196,3 +200,36 @@ def segment_prefix(row_ptr: np.ndarray, max_edges: int) -> int:
     """Number of leading centers whose segments together hold at most max_edges edges (>= 1)."""
     n = int(np.searchsorted(row_ptr, max_edges, side="right")) - 1
     return max(1, min(n, len(row_ptr) - 1))
+
+
+def layer_params(cfg: Config):
+    """Weights of one layer, float32, scaled by 1/sqrt(fan-in):
+    A [L, U], W [P, U], Mix [n_x_irreps, U, U], B1 [L + U, H], B2 [H, L]."""
+    d1, _, n_paths = dims(cfg.lmax, cfg.full_parity)
+    L, H, U = cfg.extra["L"], cfg.extra["H"], cfg.U
+    n_x = 2 * (cfg.lmax + 1) if cfg.full_parity else cfg.lmax + 1
+    rng = np.random.default_rng(seed_streams(cfg.index)[3])
+    shapes = {"A": ((L, U), L), "Mix": ((n_x, U, U), U), "B1": ((L + U, H), L + U), "B2": ((H, L), H)}
+    prm = {k: (rng.standard_normal(s) / sqrt(fan)).astype(np.float32) for k, (s, fan) in shapes.items()}
+    prm["W"] = path_weights(cfg)
+    return prm
+
+
+def layer_inputs(cfg: Config, n_edges: int, device=None):
+    """(h [E, L], V [E, U, d1], dh_out [E, L], dV_out [E, U, d1]) float32 ~ N(0, 1):
+    numpy arrays, or torch tensors drawn on `device` when it is given."""
+    d1, _, _ = dims(cfg.lmax, cfg.full_parity)
+    L, U = cfg.extra["L"], cfg.U
+    ss = seed_streams(cfg.index)
+    shapes = [(ss[1], (n_edges, L)), (ss[2], (n_edges, U, d1)), (ss[4], (n_edges, L)), (ss[0], (n_edges, U, d1))]
+    if device is None:
+        return tuple(np.random.default_rng(np.random.SeedSequence(int(c.generate_state(1)[0]) + 17))
+                     .standard_normal(shape, dtype=np.float32) for c, shape in shapes)
+    import torch
+
+    out = []
+    for child, shape in shapes:
+        g = torch.Generator(device=device)
+        g.manual_seed(int(child.generate_state(2, dtype=np.uint64)[1] & 0x7FFFFFFFFFFFFFFF))
+        out.append(torch.randn(shape, generator=g, device=device, dtype=torch.float32))
+    return tuple(out)
