@@ -191,7 +191,7 @@ def time_training_backward(torch, at, plan, inputs, grads, per_kernel_ms, reps):
             "workspace_bytes": at.allegro_tp_backward_workspace(plan, rp.numel() - 1)}
 
 
-def cpu_baseline(graph, host_inputs, max_edges=8192):
+def cpu_baseline(graph, host_inputs, max_edges=49152):
     """Time the fp64 oracle (one thread) on a prefix of whole center segments."""
     from threadpoolctl import threadpool_limits
 
