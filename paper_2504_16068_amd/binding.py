@@ -1,7 +1,7 @@
 """ctypes binding of liballegro_tp.so -- argument marshalling only.
 
 Every function here has the name of the C entry point it calls (declared in
-include/allegro_tp.h), checks tensor shapes, dtypes, devices and contiguity,
+include/allegro_tp.h and include/allegro_layer.h), checks tensor shapes, dtypes, devices and contiguity,
 allocates outputs with PyTorch when the caller passes none, and hands raw
 device pointers plus the current HIP stream to the library.  No arithmetic of
 the operation happens in Python, and there is no fallback: if the compiled
@@ -29,8 +29,11 @@ EXPORTED = (
     "allegro_tp_plan_create", "allegro_tp_plan_destroy", "allegro_tp_plan_query", "allegro_tp_plan_cg",
     "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_tp_backward_workspace",
     "allegro_tp_backward_train", "allegro_sh_forward", "allegro_sh_backward",
+    "allegro_layer_buffers", "allegro_layer_forward", "allegro_layer_backward",
     "allegro_last_error",
 )
+
+LAYER_WEIGHTS = ("A", "W", "Mix", "B1", "B2")
 
 
 class AllegroError(RuntimeError):
@@ -62,6 +65,11 @@ def _load() -> ctypes.CDLL:
     lib.allegro_tp_backward_train.argtypes = [vp, i64, i64] + [vp] * 13 + [ctypes.c_size_t, vp]
     lib.allegro_sh_forward.argtypes = [vp, i64, vp, vp, vp]
     lib.allegro_sh_backward.argtypes = [vp, i64, vp, vp, vp, vp]
+    szp = ctypes.POINTER(ctypes.c_size_t)
+    lib.allegro_layer_buffers.argtypes = [vp, i32, i32, i64, i64, szp, szp]
+    lib.allegro_layer_forward.argtypes = [vp, i32, i32, i64, i64] + [vp] * 12 + [ctypes.c_size_t, vp]
+    lib.allegro_layer_backward.argtypes = ([vp, i32, i32, i64, i64] + [vp] * 10 + [ctypes.c_size_t] + [vp] * 11
+                                           + [ctypes.c_size_t, vp])
     lib.allegro_last_error.restype = ctypes.c_char_p
     for name in EXPORTED:
         if name != "allegro_last_error":
@@ -95,6 +103,8 @@ class Plan:
         _check(_lib.allegro_tp_plan_query(self.handle, ctypes.byref(d1), ctypes.byref(d2), ctypes.byref(np_), None,
                                           ctypes.byref(nnz)))
         self.d1, self.d2, self.n_paths, self.nnz = d1.value, d2.value, np_.value, nnz.value
+        # number of x irreps: one per l, or two per l with full parity
+        self.n_x = (lmax + 1) * (2 if flags & ALLEGRO_FULL_PARITY else 1)
 
     def path_desc(self):
         buf = (ctypes.c_int * (6 * self.n_paths))()
@@ -290,3 +300,90 @@ def allegro_sh_backward(plan: Plan, vec, grad_Y, grad_vec=None, stream=None):
     _need(grad_vec, "grad_vec", (e, 3), torch.float64, dev)
     _check(_lib.allegro_sh_backward(plan.handle, e, _ptr(vec), _ptr(grad_Y), _ptr(grad_vec), _stream(stream, dev)))
     return grad_vec
+
+
+# ------------------------------------------------------------------- layer
+
+def layer_weight_shapes(plan: Plan, L: int, H: int):
+    """Shapes of the weights of one layer (include/allegro_layer.h)."""
+    return {"A": (L, plan.U), "W": (plan.n_paths, plan.U), "Mix": (plan.n_x, plan.U, plan.U),
+            "B1": (L + plan.U, H), "B2": (H, L)}
+
+
+def allegro_layer_buffers(plan: Plan, L: int, H: int, n_centers: int, n_edges: int):
+    """(saved_bytes, workspace_bytes) of one layer."""
+    sv, ws = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(_lib.allegro_layer_buffers(plan.handle, int(L), int(H), int(n_centers), int(n_edges), ctypes.byref(sv),
+                                      ctypes.byref(ws)))
+    return sv.value, ws.value
+
+
+def _bytes_buffer(t, need, name, device):
+    import torch
+
+    if t is None:
+        return torch.empty(max(need, 16), dtype=torch.uint8, device=device)
+    if t.device != torch.device(device) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous tensor on {device}")
+    return t
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def _layer_inputs(plan, L, H, row_ptr, h, V, Y, weights):
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, V.shape[0])
+    _need(h, "h", (e, L), torch.float32, dev)
+    _need(V, "V", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    for name, shape in layer_weight_shapes(plan, L, H).items():
+        _need(weights[name], name, shape, torch.float32, dev)
+    return dev, n, e
+
+
+def allegro_layer_forward(plan: Plan, L: int, H: int, row_ptr, h, V, Y, weights, h_out=None, V_out=None,
+                          saved=None, stream=None):
+    """Returns (h_out, V_out, saved); weights maps A, W, Mix, B1, B2 to device tensors."""
+    import torch
+
+    dev, n, e = _layer_inputs(plan, L, H, row_ptr, h, V, Y, weights)
+    sv_need, _ = allegro_layer_buffers(plan, L, H, n, e)
+    h_out = torch.empty_like(h) if h_out is None else h_out
+    V_out = torch.empty_like(V) if V_out is None else V_out
+    _need(h_out, "h_out", (e, L), torch.float32, dev)
+    _need(V_out, "V_out", (e, plan.U, plan.d1), torch.float32, dev)
+    saved = _bytes_buffer(saved, sv_need, "saved", dev)
+    _check(_lib.allegro_layer_forward(plan.handle, int(L), int(H), n, e, _ptr(row_ptr), _ptr(h), _ptr(V), _ptr(Y),
+                                      *(_ptr(weights[k]) for k in LAYER_WEIGHTS), _ptr(h_out), _ptr(V_out),
+                                      _ptr(saved), _nbytes(saved), _stream(stream, dev)))
+    return h_out, V_out, saved
+
+
+def allegro_layer_backward(plan: Plan, L: int, H: int, row_ptr, h, V, Y, weights, saved, dh_out, dV_out,
+                           outs=None, workspace=None, stream=None):
+    """Returns a dict of gradients: h, V, Y and the weights A, W, Mix, B1, B2."""
+    import torch
+
+    dev, n, e = _layer_inputs(plan, L, H, row_ptr, h, V, Y, weights)
+    _need(dh_out, "dh_out", (e, L), torch.float32, dev)
+    _need(dV_out, "dV_out", (e, plan.U, plan.d1), torch.float32, dev)
+    _, ws_need = allegro_layer_buffers(plan, L, H, n, e)
+    if outs is None:
+        outs = {"h": torch.empty_like(h), "V": torch.empty_like(V), "Y": torch.empty_like(Y)}
+        outs.update({k: torch.empty_like(weights[k]) for k in LAYER_WEIGHTS})
+    _need(outs["h"], "dh", (e, L), torch.float32, dev)
+    _need(outs["V"], "dV", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(outs["Y"], "dY", (e, plan.d2), torch.float32, dev)
+    for name, shape in layer_weight_shapes(plan, L, H).items():
+        _need(outs[name], "d" + name, shape, torch.float32, dev)
+    workspace = _bytes_buffer(workspace, ws_need, "workspace", dev)
+    _check(_lib.allegro_layer_backward(plan.handle, int(L), int(H), n, e, _ptr(row_ptr), _ptr(h), _ptr(V), _ptr(Y),
+                                       *(_ptr(weights[k]) for k in LAYER_WEIGHTS), _ptr(saved), _nbytes(saved),
+                                       _ptr(dh_out), _ptr(dV_out), _ptr(outs["h"]), _ptr(outs["V"]), _ptr(outs["Y"]),
+                                       *(_ptr(outs[k]) for k in LAYER_WEIGHTS), _ptr(workspace), _nbytes(workspace),
+                                       _stream(stream, dev)))
+    return outs

@@ -4,8 +4,8 @@ Steps (every call rebuilds everything):
   1. g++ compiles the C++ coupling-table builder into the generator and runs it,
      writing csrc/generated/tp_cores.inc (straight-line contraction cores);
   2. g++ compiles the builder for the library (host code, -fPIC);
-  3. hipcc compiles the kernels and the C ABI for gfx950, with packed-fp32
-     instruction selection disabled;
+  3. hipcc compiles the kernels and the C ABI for gfx950 (the tensor product,
+     then the layer around it), with packed-fp32 instruction selection disabled;
   4. hipcc links liballegro_tp.so next to this file.
 The per-kernel register / scratch report of step 3 is written to
 _build/resource_usage.txt; a kernel that spills to scratch fails the build.
@@ -27,6 +27,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liballegro_tp.so")
 ARCH = "gfx950"
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+HIP_SOURCES = ("allegro_tp.hip", "allegro_layer.hip")  # tensor product; the layer around it
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
              "-I", os.path.join(ROOT, "include"), "-I", CSRC]
@@ -72,16 +73,20 @@ def build(verbose: bool = False) -> str:
     _run([gen_exe, os.path.join(GEN, "tp_cores.inc")])
     cg_obj = os.path.join(BUILD, "cg_builder.o")
     _run(["g++", "-O2", "-std=c++17", "-fPIC", "-c", os.path.join(CSRC, "cg_builder.cpp"), "-o", cg_obj])
-    hip_obj = os.path.join(BUILD, "allegro_tp.o")
-    res = _run([HIPCC, *HIP_FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c",
-                os.path.join(CSRC, "allegro_tp.hip"), "-o", hip_obj])
-    summary, spills = _check_resources(res.stderr)
+    objs, report = [], ""
+    for src in HIP_SOURCES:
+        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        res = _run([HIPCC, *HIP_FLAGS, "-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src),
+                    "-o", obj])
+        objs.append(obj)
+        report += res.stderr
+    summary, spills = _check_resources(report)
     with open(os.path.join(BUILD, "resource_usage.txt"), "w") as f:
         f.write(summary)
     if spills:
         raise RuntimeError("kernels use scratch memory (see _build/resource_usage.txt): " + ", ".join(spills))
     tmp = LIB + ".tmp"
-    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", hip_obj, cg_obj, "-o", tmp])
+    _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, cg_obj, "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print(summary)

@@ -1,0 +1,728 @@
+// MI355X (gfx950) kernels and C ABI of one Allegro layer around the tensor
+// product.  What is computed is stated in include/allegro_layer.h.
+//
+// The dense contractions run on the fp32 matrix cores with
+// v_mfma_f32_16x16x4_f32: for one instruction lane l supplies A[l % 16][l / 16]
+// and B[l / 16][l % 16], and accumulator register r of lane l holds
+// D[4 (l / 16) + r][l % 16].  Over the steps of a sum, lane group l / 16
+// either interleaves with the others (k = 4 s + l / 16) or owns a contiguous
+// quarter of k, whichever keeps that kernel's LDS reads free of bank
+// conflicts; A and B always use the same order, so every product pairs the
+// same k.
+//
+//   row_gemm_kernel     C[E][N] = X[E][K] B[K][N], X = [x1 | x2] staged in LDS,
+//                       with a fused prologue (SiLU) and epilogue (add,
+//                       SiLU-gradient scale, column split): w = h A,
+//                       a = [h, s] B1, h' = h + SiLU(a) B2 and their VJPs
+//   reduce_gemm_kernel  G[M][N] = sum_e P[e][M] Q[e][N] (dA, dB1, dB2):
+//                       persistent workgroups with register accumulators,
+//                       one partial per workgroup, then colsum_kernel
+//   mix_kernel          per-irrep channel mixing V' = Mix_c T_c (forward) or
+//                       dT = Mix_c^T dV' (backward); each wave keeps its 16
+//                       output channels' rows of every Mix_c in registers
+//   mix_wgrad_kernel    dMix_c = sum over edges and components of dV'_c T_c^T
+//   colsum_kernel       fixed-order sum of the workgroups' partials
+//
+// Edge-major [E][U][d1] tiles are staged through LDS in a per-irrep column
+// layout: column (e, m) of irrep c holds the U channels of component
+// off(c) + m of edge e, columns padded so that the 64 lanes of an MFMA
+// operand read hit distinct banks.  All reductions over edges have a fixed
+// order and no atomics, so every output is bit-identical run to run.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <type_traits>
+
+#include "allegro_layer.h"
+#include "device_common.hpp"
+#include "plan.hpp"
+
+namespace {
+
+using namespace allegro_dev;
+using allegro_internal::fail;
+
+constexpr int kWave = 64;
+constexpr int kThreads = 256;  // four waves per workgroup
+constexpr int kU = 64;         // channels supported by the layer
+
+__device__ __forceinline__ f32x4 mfma_16x16x4(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// SiLU(a) = a / (1 + exp(-a)) and its derivative sigma(a) (1 + a (1 - sigma(a))).
+__device__ __forceinline__ float silu(float a) { return a / (1.0f + expf(-a)); }
+__device__ __forceinline__ float silu_grad(float a) {
+  const float sg = 1.0f / (1.0f + expf(-a));
+  return sg * (1.0f + a * (1.0f - sg));
+}
+
+template <int C, int END, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (C < END) {
+    f(std::integral_constant<int, C>{});
+    static_for<C + 1, END>(f);
+  }
+}
+
+// The x irreps of a plan: for l = 0..lmax, (l, natural parity) then, with
+// full parity, (l, the other parity); sizes 2l + 1, concatenated.
+template <int LMAX, bool FULL>
+struct XIrreps {
+  static constexpr int NX = FULL ? 2 * (LMAX + 1) : LMAX + 1;
+  static constexpr int D1 = FULL ? 2 * (LMAX + 1) * (LMAX + 1) : (LMAX + 1) * (LMAX + 1);
+  static constexpr int dim(int c) { return 2 * (FULL ? c / 2 : c) + 1; }
+  static constexpr int off(int c) { return c == 0 ? 0 : off(c - 1) + dim(c - 1); }
+};
+
+// ------------------------------------------------------------- row GEMM
+enum { kProNone = 0, kProSilu = 1 };
+enum { kEpiStore = 0, kEpiAdd = 1, kEpiSiluGrad = 2, kEpiSplitAdd = 3 };
+
+struct RowGemmArgs {
+  int64_t E;
+  const float *x1, *x2;  // X = [x1 | x2], [E][K1] and [E][K2]
+  const float *b;        // B[k][n] = b[k * b_rs + n * b_cs]
+  int b_rs, b_cs;
+  const float *d;        // addend (kEpiAdd, kEpiSplitAdd) or pre-activation (kEpiSiluGrad)
+  float *c, *c2;         // output; kEpiSplitAdd: columns < N1 to c, the rest to c2
+};
+
+constexpr int kRowTile = 64;  // rows per workgroup tile; wave w owns rows 16w .. 16w+15
+
+template <int KX, int PRO>
+__device__ __forceinline__ void stage_rows(const float *__restrict__ x, int64_t r0, int rows, float *xs, int XS,
+                                           int col0, int tid) {
+  for (int f = tid; f < kRowTile * KX / 4; f += kThreads) {
+    const int r = f / (KX / 4), k = 4 * (f % (KX / 4));
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < rows) v = *reinterpret_cast<const float4 *>(x + (r0 + r) * KX + k);
+    if constexpr (PRO == kProSilu) {
+      v.x = silu(v.x); v.y = silu(v.y); v.z = silu(v.z); v.w = silu(v.w);
+    }
+    *reinterpret_cast<float4 *>(xs + r * XS + col0 + k) = v;
+  }
+}
+
+template <int K1, int K2, int N, int N1, int PRO, int EPI>
+__global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
+  constexpr int K = K1 + K2, XS = K + 4;  // row stride: the 16 rows of an A read hit distinct banks
+  static_assert(K1 % 16 == 0 && K2 % 16 == 0 && N % 16 == 0 && N1 % 16 == 0, "tile shape");
+  __shared__ float4 xs4[kRowTile * XS / 4];
+  float *xs = reinterpret_cast<float *>(xs4);
+  const int tid = threadIdx.x, wave = tid / kWave, l = tid % kWave;
+  const int64_t n_tiles = (g.E + kRowTile - 1) / kRowTile;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int64_t r0 = t * kRowTile;
+    const int rows = int(g.E - r0 < kRowTile ? g.E - r0 : kRowTile);
+    stage_rows<K1, PRO>(g.x1, r0, rows, xs, XS, 0, tid);
+    if constexpr (K2 > 0) stage_rows<K2, kProNone>(g.x2, r0, rows, xs, XS, K1, tid);
+    lds_sync<4>();
+    // step s pairs k = 4 s + l / 16 (with XS = 4 (mod 64) the 64 lanes of an A read hit distinct banks)
+    const float *xa = xs + (16 * wave + l % 16) * XS + l / 16;
+#pragma unroll 1
+    for (int ct = 0; ct < N / 16; ++ct) {
+      const int n = 16 * ct + l % 16;
+      const float *bb = g.b + (l / 16) * g.b_rs + n * g.b_cs;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < K / 4; ++s) acc = mfma_16x16x4(xa[4 * s], bb[4 * s * g.b_rs], acc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * wave + 4 * (l / 16) + r;
+        if (row >= rows) continue;
+        const int64_t e = r0 + row;
+        if constexpr (EPI == kEpiStore) {
+          g.c[e * N + n] = acc[r];
+        } else if constexpr (EPI == kEpiAdd) {
+          g.c[e * N + n] = acc[r] + g.d[e * N + n];
+        } else if constexpr (EPI == kEpiSiluGrad) {
+          g.c[e * N + n] = acc[r] * silu_grad(g.d[e * N + n]);
+        } else {
+          if (16 * ct < N1) g.c[e * N1 + n] = acc[r] + g.d[e * N1 + n];
+          else g.c2[e * (N - N1) + (n - N1)] = acc[r];
+        }
+      }
+    }
+    lds_sync<4>();
+  }
+}
+
+// ---------------------------------------------------------- reduce GEMM
+constexpr int kRedTile = 64;  // edges per step
+
+template <int M1, int M2, int N, int PRO>
+__global__ __launch_bounds__(kThreads) void reduce_gemm_kernel(int64_t E, const float *__restrict__ p1,
+                                                               const float *__restrict__ p2,
+                                                               const float *__restrict__ q,
+                                                               float *__restrict__ part) {
+  constexpr int M = M1 + M2, PS = M + 16, QS = N + 16;  // strides = 16 (mod 64): conflict-free operand reads
+  constexpr int MT = M / 16, NJ = N / 64;  // wave w owns column tiles nt = w + 4 j (j < NJ) of every row tile
+  static_assert(M1 % 16 == 0 && M2 % 16 == 0 && N % 64 == 0, "tile shape");
+  __shared__ float4 ps4[kRedTile * PS / 4], qs4[kRedTile * QS / 4];
+  float *ps = reinterpret_cast<float *>(ps4), *qs = reinterpret_cast<float *>(qs4);
+  const int tid = threadIdx.x, wave = tid / kWave, l = tid % kWave;
+  f32x4 acc[MT][NJ];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t n_tiles = (E + kRedTile - 1) / kRedTile;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int64_t r0 = t * kRedTile;
+    const int rows = int(E - r0 < kRedTile ? E - r0 : kRedTile);
+    stage_rows<M1, PRO>(p1, r0, rows, ps, PS, 0, tid);
+    if constexpr (M2 > 0) stage_rows<M2, kProNone>(p2, r0, rows, ps, PS, M1, tid);
+    stage_rows<N, kProNone>(q, r0, rows, qs, QS, 0, tid);
+    lds_sync<4>();
+    // the sum runs over the tile's edges: step s pairs edge 4 s + l / 16
+    const float *pa = ps + (l / 16) * PS + l % 16;
+    const float *qb = qs + (l / 16) * QS + 16 * wave + l % 16;
+#pragma unroll 2
+    for (int s = 0; s < kRedTile / 4; ++s) {
+      float a[MT], b[NJ];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) a[mt] = pa[4 * s * PS + 16 * mt];
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) b[j] = qb[4 * s * QS + 64 * j];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[mt][j] = mfma_16x16x4(a[mt], b[j], acc[mt][j]);
+    }
+    lds_sync<4>();
+  }
+  float *out = part + int64_t(blockIdx.x) * M * N;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int j = 0; j < NJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        out[(16 * mt + 4 * (l / 16) + r) * N + 16 * (wave + 4 * j) + l % 16] = acc[mt][j][r];
+}
+
+__global__ __launch_bounds__(256) void colsum_kernel(int R, int C, const float *__restrict__ part,
+                                                     float *__restrict__ out) {
+  const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (c >= C) return;
+  float a = 0.0f;
+  for (int r = 0; r < R; ++r) a += part[int64_t(r) * C + c];
+  out[c] = a;
+}
+
+// ------------------------------------------------------------ mixing
+// LDS column index of component k of edge e in a tile of ne_tile edges.
+template <class X>
+__device__ __forceinline__ void component_column(int k, int ne_tile, int &col0, int &dim) {
+  int c = 0;
+#pragma unroll
+  for (int i = 1; i < X::NX; ++i) c = k >= X::off(i) ? i : c;
+  int o = 0, d = 1;
+#pragma unroll
+  for (int i = 0; i < X::NX; ++i)
+    if (i == c) { o = X::off(i); d = X::dim(i); }
+  col0 = ne_tile * o + (k - o);
+  dim = d;
+}
+
+constexpr int kMixEdges = 8;  // edges per tile
+constexpr int kMixCS = kU + 1;  // column stride: 16 consecutive columns hit distinct banks
+constexpr int kChunk = 8;       // float4 per thread in flight while a tile is staged
+
+template <int LMAX, bool FULL, bool BWD>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void mix_kernel(
+    int64_t E, const float *__restrict__ src, const float *__restrict__ mix, const float *__restrict__ ds,
+    float *__restrict__ dst, float *__restrict__ s_out) {
+  using X = XIrreps<LMAX, FULL>;
+  constexpr int U = kU, D1 = X::D1, NX = X::NX, NE = kMixEdges, CS = kMixCS;
+  constexpr int COLS = NE * D1, F4 = NE * U * D1 / 4, PER = (F4 + kThreads - 1) / kThreads;
+  static_assert((U * D1) % 4 == 0, "edge rows must be whole float4");
+  // +16 columns: the last irrep's padded column tile reads past its columns
+  __shared__ float lds[(COLS + 16) * CS];
+  __shared__ int kcol[D1], kdim[D1];
+  const int tid = threadIdx.x, w = tid / kWave, l = tid % kWave;
+  if (tid < D1) component_column<X>(tid, NE, kcol[tid], kdim[tid]);
+  // A operands: wave w's output rows 16w .. 16w+15 of every Mix_c (or Mix_c^T)
+  float A[NX][16];
+  static_for<0, NX>([&](auto ic) {
+    constexpr int c = decltype(ic)::value;
+#pragma unroll
+    for (int s = 0; s < 16; ++s)
+      A[c][s] = BWD ? mix[(c * U + 16 * (l / 16) + s) * U + 16 * w + l % 16]
+                    : mix[(c * U + 16 * w + l % 16) * U + 16 * (l / 16) + s];
+  });
+  lds_sync<4>();
+  const int64_t n_tiles = (E + NE - 1) / NE;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int64_t e0 = t * NE;
+    const int ne = int(E - e0 < NE ? E - e0 : NE);
+    const int nf4 = ne * (U * D1 / 4);
+    const float4 *s4 = reinterpret_cast<const float4 *>(src + e0 * U * D1);
+#pragma unroll 1
+    for (int i0 = 0; i0 < PER; i0 += kChunk) {
+      float4 v[kChunk];
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int f = tid + kThreads * (i0 + i);
+        v[i] = f < nf4 ? load_stream(s4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int f = tid + kThreads * (i0 + i);
+        if (f >= F4) continue;
+        const float vv[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int idx = 4 * f + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
+          lds[(kcol[k] + e * kdim[k]) * CS + u] = vv[q];
+        }
+      }
+    }
+    lds_sync<4>();
+    if constexpr (!BWD) {
+      // s[e][u] = T[e][u][0]: irrep 0 (0e) has one component, so its column is e
+      for (int i = tid; i < ne * U; i += kThreads) s_out[(e0 + i / U) * U + i % U] = lds[(i / U) * CS + i % U];
+    }
+    static_for<0, NX>([&](auto ic) {
+      constexpr int c = decltype(ic)::value, nq = NE * X::dim(c), NCT = (nq + 15) / 16, base = NE * X::off(c);
+      f32x4 acc[NCT];
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const float *bp = lds + (base + 16 * ct + l % 16) * CS + 16 * (l / 16);
+        acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 16; ++s) acc[ct] = mfma_16x16x4(A[c][s], bp[s], acc[ct]);
+      }
+      lds_sync<4>();  // every wave has read irrep c's columns
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const int q = 16 * ct + l % 16;
+        if (q >= nq) continue;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int uo = 16 * w + 4 * (l / 16) + r;
+          float val = acc[ct][r];
+          if constexpr (BWD && c == 0) {
+            if (q < ne) val += ds[(e0 + q) * U + uo];
+          }
+          lds[(base + q) * CS + uo] = val;
+        }
+      }
+    });
+    lds_sync<4>();
+    float4 *d4 = reinterpret_cast<float4 *>(dst + e0 * U * D1);
+#pragma unroll 1
+    for (int i0 = 0; i0 < PER; i0 += kChunk) {
+#pragma unroll
+      for (int i = 0; i < kChunk; ++i) {
+        const int f = tid + kThreads * (i0 + i);
+        if (f >= nf4) continue;
+        float vv[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int idx = 4 * f + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
+          vv[q] = lds[(kcol[k] + e * kdim[k]) * CS + u];
+        }
+        store_stream(make_float4(vv[0], vv[1], vv[2], vv[3]), d4 + f);
+      }
+    }
+    lds_sync<4>();
+  }
+}
+
+constexpr int kWgEdges = 4;        // edges per tile: column counts NE * (2l + 1) are multiples of 4
+constexpr int kWgCS = kU + 16;     // = 16 (mod 64): the four lane groups of an operand read hit distinct banks
+
+template <int LMAX, bool FULL>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void mix_wgrad_kernel(
+    int64_t E, const float *__restrict__ dv, const float *__restrict__ tt, float *__restrict__ part) {
+  using X = XIrreps<LMAX, FULL>;
+  constexpr int U = kU, D1 = X::D1, NX = X::NX, NE = kWgEdges, CS = kWgCS;
+  constexpr int COLS = NE * D1, F4 = NE * U * D1 / 4, PER = (F4 + kThreads - 1) / kThreads;
+  static_assert((U * D1) % 4 == 0, "edge rows must be whole float4");
+  __shared__ float la[COLS * CS], lb[COLS * CS];
+  const int tid = threadIdx.x, w = tid / kWave, l = tid % kWave;
+  // every tile puts the thread's elements at the same LDS addresses
+  int addr[PER][4];
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = 4 * (tid + kThreads * i) + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1,
+                k = rem % D1;
+      int col0, dim;
+      component_column<X>(k, NE, col0, dim);
+      addr[i][q] = (col0 + e * dim) * CS + u;
+    }
+  f32x4 acc[NX][4];
+#pragma unroll
+  for (int c = 0; c < NX; ++c)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t n_tiles = (E + NE - 1) / NE;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    const int64_t e0 = t * NE;
+    const int ne = int(E - e0 < NE ? E - e0 : NE);
+    const int nf4 = ne * (U * D1 / 4);
+    const float4 *a4 = reinterpret_cast<const float4 *>(dv + e0 * U * D1);
+    const float4 *b4 = reinterpret_cast<const float4 *>(tt + e0 * U * D1);
+    float4 va[PER], vb[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = tid + kThreads * i;
+      va[i] = f < nf4 ? load_stream(a4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+      vb[i] = f < nf4 ? load_stream(b4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (tid + kThreads * i >= F4) continue;
+      la[addr[i][0]] = va[i].x; la[addr[i][1]] = va[i].y; la[addr[i][2]] = va[i].z; la[addr[i][3]] = va[i].w;
+      lb[addr[i][0]] = vb[i].x; lb[addr[i][1]] = vb[i].y; lb[addr[i][2]] = vb[i].z; lb[addr[i][3]] = vb[i].w;
+    }
+    lds_sync<4>();
+    // dMix_c[v][u] += sum_q dV'_c[q][v] T_c[q][u]; lane group l / 16 owns
+    // the quarter of the irrep's columns q = (l / 16) * nq / 4 + s
+    static_for<0, NX>([&](auto ic) {
+      constexpr int c = decltype(ic)::value, nq = NE * X::dim(c), base = NE * X::off(c);
+      const int q0 = base + (l / 16) * (nq / 4);
+#pragma unroll
+      for (int s = 0; s < nq / 4; ++s) {
+        const float a = la[(q0 + s) * CS + 16 * w + l % 16];
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[c][nt] = mfma_16x16x4(a, lb[(q0 + s) * CS + 16 * nt + l % 16], acc[c][nt]);
+      }
+    });
+    lds_sync<4>();
+  }
+  float *out = part + int64_t(blockIdx.x) * NX * U * U;
+#pragma unroll
+  for (int c = 0; c < NX; ++c)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        out[(c * U + 16 * w + 4 * (l / 16) + r) * U + 16 * nt + l % 16] = acc[c][nt][r];
+}
+
+// ------------------------------------------------------------- host side
+constexpr int64_t kMaxPersistent = 512;  // workgroups of the persistent kernels (2 per CU)
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+int64_t red_groups(int64_t E) { return std::min<int64_t>(cdiv(E, kRedTile), kMaxPersistent); }
+int64_t wgrad_groups(int64_t E) { return std::min<int64_t>(cdiv(E, kWgEdges), kMaxPersistent); }
+
+struct Shape {
+  int L = 0, H = 0, U = 0, d1 = 0, d2 = 0, P = 0, NX = 0;
+  int64_t N = 0, E = 0;
+};
+
+// Byte offsets of the regions of the saved and workspace buffers.
+struct SavedLayout {
+  size_t w, env, T, s, a, total;
+};
+struct WorkLayout {
+  size_t dT, da, dhm, ds, dw, genv, tpws, red, mixp, total, tpws_bytes;
+};
+
+SavedLayout saved_layout(const Shape &z) {
+  SavedLayout o{};
+  size_t at = 0;
+  auto take = [&](size_t floats) { const size_t off = at; at += align256(floats * sizeof(float)); return off; };
+  o.w = take(size_t(z.E) * z.U);
+  o.env = take(size_t(z.N) * z.U * z.d2);
+  o.T = take(size_t(z.E) * z.U * z.d1);
+  o.s = take(size_t(z.E) * z.U);
+  o.a = take(size_t(z.E) * z.H);
+  o.total = at;
+  return o;
+}
+
+WorkLayout work_layout(const allegro_tp_plan *plan, const Shape &z) {
+  WorkLayout o{};
+  size_t at = 0;
+  auto take = [&](size_t bytes) { const size_t off = at; at += align256(bytes); return off; };
+  const size_t f = sizeof(float);
+  o.dT = take(size_t(z.E) * z.U * z.d1 * f);
+  o.da = take(size_t(z.E) * z.H * f);
+  o.dhm = take(size_t(z.E) * z.L * f);
+  o.ds = take(size_t(z.E) * z.U * f);
+  o.dw = take(size_t(z.E) * z.U * f);
+  o.genv = take(size_t(z.N) * z.U * z.d2 * f);
+  size_t tpws = 0;
+  (void)allegro_tp_backward_workspace(plan, z.N, &tpws);
+  o.tpws_bytes = tpws;
+  o.tpws = take(tpws);
+  const size_t mn = std::max({size_t(z.L + z.U) * z.H, size_t(z.H) * z.L, size_t(z.L) * z.U});
+  o.red = take(size_t(red_groups(z.E)) * mn * f);
+  o.mixp = take(size_t(wgrad_groups(z.E)) * z.NX * z.U * z.U * f);
+  o.total = at;
+  return o;
+}
+
+int after(const char *what) {
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(ALLEGRO_E_HIP, "%s launch failed: %s", what, hipGetErrorString(err));
+  return ALLEGRO_OK;
+}
+
+unsigned row_grid(int64_t E) { return unsigned(std::min<int64_t>(cdiv(E, kRowTile), 8192)); }
+
+void colsum(hipStream_t s, int64_t R, int C, const float *part, float *out) {
+  hipLaunchKernelGGL(colsum_kernel, dim3(unsigned(cdiv(C, 256))), dim3(256), 0, s, int(R), C, part, out);
+}
+
+// Launchers of the dense contractions of a layer with latent width L and hidden width H.
+template <int L, int H>
+struct DenseOps {
+  static constexpr int U = kU;
+  template <int K1, int K2, int N, int N1, int PRO, int EPI>
+  static void row(hipStream_t s, const RowGemmArgs &g) {
+    if (g.E == 0) return;
+    hipLaunchKernelGGL((row_gemm_kernel<K1, K2, N, N1, PRO, EPI>), dim3(row_grid(g.E)), dim3(kThreads), 0, s, g);
+  }
+  template <int M1, int M2, int N, int PRO>
+  static void reduce(hipStream_t s, int64_t E, const float *p1, const float *p2, const float *q, float *part,
+                     float *out) {
+    const int64_t G = red_groups(E);
+    if (G > 0)
+      hipLaunchKernelGGL((reduce_gemm_kernel<M1, M2, N, PRO>), dim3(unsigned(G)), dim3(kThreads), 0, s, E, p1, p2, q,
+                         part);
+    colsum(s, G, (M1 + M2) * N, part, out);
+  }
+
+  // w = h A;  a = [h, s] B1 (after the mixing has written s);  h' = h + SiLU(a) B2
+  static void embed_weights(hipStream_t s, int64_t E, const float *h, const float *A, float *w) {
+    row<L, 0, U, 0, kProNone, kEpiStore>(s, {E, h, nullptr, A, U, 1, nullptr, w, nullptr});
+  }
+  static void latent(hipStream_t s, int64_t E, const float *h, const float *sv, const float *B1, const float *B2,
+                     float *a, float *h_out) {
+    row<L, U, H, 0, kProNone, kEpiStore>(s, {E, h, sv, B1, H, 1, nullptr, a, nullptr});
+    row<H, 0, L, 0, kProSilu, kEpiAdd>(s, {E, a, nullptr, B2, L, 1, h, h_out, nullptr});
+  }
+  // da = (dh' B2^T) * SiLU'(a);  [dhm | ds] = [dh', 0] + da B1^T;  dB2, dB1
+  static void latent_vjp(hipStream_t s, int64_t E, const float *h, const float *sv, const float *a,
+                         const float *B1, const float *B2, const float *dh_out, float *da, float *dhm, float *ds,
+                         float *part, float *dB1, float *dB2) {
+    row<L, 0, H, 0, kProNone, kEpiSiluGrad>(s, {E, dh_out, nullptr, B2, 1, L, a, da, nullptr});
+    row<H, 0, L + U, L, kProNone, kEpiSplitAdd>(s, {E, da, nullptr, B1, 1, H, dh_out, dhm, ds});
+    reduce<H, 0, L, kProSilu>(s, E, a, nullptr, dh_out, part, dB2);
+    reduce<L, U, H, kProNone>(s, E, h, sv, da, part, dB1);
+  }
+  // dA = h^T dw;  dh = dhm + dw A^T
+  static void embed_vjp(hipStream_t s, int64_t E, const float *h, const float *A, const float *dw, const float *dhm,
+                        float *part, float *dA, float *dh) {
+    reduce<L, 0, U, kProNone>(s, E, h, nullptr, dw, part, dA);
+    row<U, 0, L, 0, kProNone, kEpiAdd>(s, {E, dw, nullptr, A, 1, U, dhm, dh, nullptr});
+  }
+};
+
+struct DenseTable {
+  void (*embed_weights)(hipStream_t, int64_t, const float *, const float *, float *) = nullptr;
+  void (*latent)(hipStream_t, int64_t, const float *, const float *, const float *, const float *, float *,
+                 float *) = nullptr;
+  void (*latent_vjp)(hipStream_t, int64_t, const float *, const float *, const float *, const float *,
+                     const float *, const float *, float *, float *, float *, float *, float *, float *) = nullptr;
+  void (*embed_vjp)(hipStream_t, int64_t, const float *, const float *, const float *, const float *, float *,
+                    float *, float *) = nullptr;
+};
+
+template <int L, int H>
+DenseTable dense_table() {
+  using D = DenseOps<L, H>;
+  return {&D::embed_weights, &D::latent, &D::latent_vjp, &D::embed_vjp};
+}
+
+DenseTable select_dense(int L, int H) {
+  if (L == 64 && H == 64) return dense_table<64, 64>();
+  if (L == 64 && H == 128) return dense_table<64, 128>();
+  if (L == 128 && H == 64) return dense_table<128, 64>();
+  if (L == 128 && H == 128) return dense_table<128, 128>();
+  return {};
+}
+
+// Launchers of the mixing kernels of one (lmax, parity).
+template <int LMAX, bool FULL>
+struct MixOps {
+  static void forward(hipStream_t s, int64_t E, const float *T, const float *mix, float *V_out, float *sv) {
+    if (E == 0) return;
+    const unsigned G = unsigned(std::min<int64_t>(cdiv(E, kMixEdges), kMaxPersistent));
+    hipLaunchKernelGGL((mix_kernel<LMAX, FULL, false>), dim3(G), dim3(kThreads), 0, s, E, T, mix, nullptr, V_out,
+                       sv);
+  }
+  static void backward(hipStream_t s, int64_t E, const float *dV_out, const float *T, const float *mix,
+                       const float *ds, float *dT, float *part, float *dmix) {
+    using X = XIrreps<LMAX, FULL>;
+    const int64_t Gw = wgrad_groups(E);
+    if (E > 0) {
+      const unsigned G = unsigned(std::min<int64_t>(cdiv(E, kMixEdges), kMaxPersistent));
+      hipLaunchKernelGGL((mix_kernel<LMAX, FULL, true>), dim3(G), dim3(kThreads), 0, s, E, dV_out, mix, ds, dT,
+                         nullptr);
+      hipLaunchKernelGGL((mix_wgrad_kernel<LMAX, FULL>), dim3(unsigned(Gw)), dim3(kThreads), 0, s, E, dV_out, T,
+                         part);
+    }
+    colsum(s, Gw, X::NX * kU * kU, part, dmix);
+  }
+};
+
+struct MixTable {
+  void (*forward)(hipStream_t, int64_t, const float *, const float *, float *, float *) = nullptr;
+  void (*backward)(hipStream_t, int64_t, const float *, const float *, const float *, const float *, float *,
+                   float *, float *) = nullptr;
+};
+
+template <int LMAX, bool FULL>
+MixTable mix_table() {
+  return {&MixOps<LMAX, FULL>::forward, &MixOps<LMAX, FULL>::backward};
+}
+
+MixTable select_mix(int lmax, bool full) {
+  switch (lmax * 2 + (full ? 1 : 0)) {
+    case 2: return mix_table<1, false>();
+    case 3: return mix_table<1, true>();
+    case 4: return mix_table<2, false>();
+    case 5: return mix_table<2, true>();
+    case 6: return mix_table<3, false>();
+    case 7: return mix_table<3, true>();
+    default: return {};
+  }
+}
+
+int layer_shape(const allegro_tp_plan *plan, int L, int H, int64_t N, int64_t E, Shape &z) {
+  if (!plan) return fail(ALLEGRO_E_INVALID, "plan is NULL");
+  if (N < 0 || E < 0) return fail(ALLEGRO_E_INVALID, "negative size (N=%lld, E=%lld)", (long long)N, (long long)E);
+  if (N == 0 && E > 0) return fail(ALLEGRO_E_INVALID, "E=%lld edges but N=0 centers", (long long)E);
+  if (N >= (int64_t(1) << 31)) return fail(ALLEGRO_E_INVALID, "N=%lld exceeds 2^31-1", (long long)N);
+  if (plan->U != kU) return fail(ALLEGRO_E_UNSUPPORTED, "the layer supports U=64 (plan has U=%d)", plan->U);
+  if (!select_dense(L, H).latent)
+    return fail(ALLEGRO_E_UNSUPPORTED, "the layer supports L, H in {64, 128} (got L=%d, H=%d)", L, H);
+  const auto &t = plan->table;
+  z.L = L;
+  z.H = H;
+  z.U = plan->U;
+  z.d1 = t.d1;
+  z.d2 = t.d2;
+  z.P = int(t.paths.size());
+  z.NX = int(t.x_irreps.size());
+  z.N = N;
+  z.E = E;
+  return ALLEGRO_OK;
+}
+
+int check_ptr(const void *p, const char *name) {
+  if (!p) return fail(ALLEGRO_E_INVALID, "%s is NULL", name);
+  if (reinterpret_cast<uintptr_t>(p) & 15u) return fail(ALLEGRO_E_INVALID, "%s is not 16-byte aligned", name);
+  return ALLEGRO_OK;
+}
+
+template <class T>
+T *at(void *base, size_t off) {
+  return reinterpret_cast<T *>(static_cast<char *>(base) + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+int allegro_layer_buffers(const allegro_tp_plan *plan, int L, int H, int64_t N, int64_t E, size_t *saved_bytes,
+                          size_t *workspace_bytes) {
+  Shape z;
+  int rc = layer_shape(plan, L, H, N, E, z);
+  if (rc) return rc;
+  if (saved_bytes) *saved_bytes = saved_layout(z).total;
+  if (workspace_bytes) *workspace_bytes = work_layout(plan, z).total;
+  return ALLEGRO_OK;
+}
+
+int allegro_layer_forward(const allegro_tp_plan *plan, int L, int H, int64_t N, int64_t E, const int64_t *row_ptr,
+                          const float *h, const float *V, const float *Y, const float *A, const float *W,
+                          const float *Mix, const float *B1, const float *B2, float *h_out, float *V_out,
+                          void *saved, size_t saved_bytes, void *stream) {
+  Shape z;
+  int rc = layer_shape(plan, L, H, N, E, z);
+  if (rc) return rc;
+  if (N == 0) return ALLEGRO_OK;
+  const SavedLayout sl = saved_layout(z);
+  if ((rc = check_ptr(saved, "saved"))) return rc;
+  if (saved_bytes < sl.total)
+    return fail(ALLEGRO_E_INVALID, "saved buffer of %zu bytes is smaller than the %zu required", saved_bytes,
+                sl.total);
+  if ((rc = check_ptr(W, "W")) || (rc = check_ptr(A, "A")) || (rc = check_ptr(Mix, "Mix")) ||
+      (rc = check_ptr(B1, "B1")) || (rc = check_ptr(B2, "B2")))
+    return rc;
+  if (E > 0 && ((rc = check_ptr(h, "h")) || (rc = check_ptr(V, "V")) || (rc = check_ptr(Y, "Y")) ||
+                (rc = check_ptr(h_out, "h_out")) || (rc = check_ptr(V_out, "V_out"))))
+    return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const DenseTable dn = select_dense(L, H);
+  const MixTable mx = select_mix(plan->lmax, (plan->flags & ALLEGRO_FULL_PARITY) != 0);
+  if (!mx.forward) return fail(ALLEGRO_E_UNSUPPORTED, "no mixing kernel for this plan");
+  float *w = at<float>(saved, sl.w), *env = at<float>(saved, sl.env), *T = at<float>(saved, sl.T);
+  float *sv = at<float>(saved, sl.s), *a = at<float>(saved, sl.a);
+  dn.embed_weights(s, E, h, A, w);
+  if ((rc = after("allegro_layer_forward"))) return rc;
+  if ((rc = allegro_env_embed(plan, N, E, row_ptr, w, Y, env, stream))) return rc;
+  if ((rc = allegro_tp_forward(plan, N, E, row_ptr, V, env, W, T, stream))) return rc;
+  mx.forward(s, E, T, Mix, V_out, sv);
+  dn.latent(s, E, h, sv, B1, B2, a, h_out);
+  return after("allegro_layer_forward");
+}
+
+int allegro_layer_backward(const allegro_tp_plan *plan, int L, int H, int64_t N, int64_t E, const int64_t *row_ptr,
+                           const float *h, const float *V, const float *Y, const float *A, const float *W,
+                           const float *Mix, const float *B1, const float *B2, const void *saved, size_t saved_bytes,
+                           const float *dh_out, const float *dV_out, float *dh, float *dV, float *dY, float *dA,
+                           float *dW, float *dMix, float *dB1, float *dB2, void *workspace, size_t workspace_bytes,
+                           void *stream) {
+  Shape z;
+  int rc = layer_shape(plan, L, H, N, E, z);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if ((rc = check_ptr(dA, "dA")) || (rc = check_ptr(dW, "dW")) || (rc = check_ptr(dMix, "dMix")) ||
+      (rc = check_ptr(dB1, "dB1")) || (rc = check_ptr(dB2, "dB2")) || (rc = check_ptr(W, "W")) ||
+      (rc = check_ptr(A, "A")) || (rc = check_ptr(Mix, "Mix")) || (rc = check_ptr(B1, "B1")) ||
+      (rc = check_ptr(B2, "B2")))
+    return rc;
+  if (N == 0) {  // no centers, no edges: every weight gradient is zero
+    colsum(s, 0, z.L * z.U, nullptr, dA);
+    colsum(s, 0, z.P * z.U, nullptr, dW);
+    colsum(s, 0, z.NX * z.U * z.U, nullptr, dMix);
+    colsum(s, 0, (z.L + z.U) * z.H, nullptr, dB1);
+    colsum(s, 0, z.H * z.L, nullptr, dB2);
+    return after("allegro_layer_backward");
+  }
+  const SavedLayout sl = saved_layout(z);
+  const WorkLayout wl = work_layout(plan, z);
+  if ((rc = check_ptr(saved, "saved")) || (rc = check_ptr(workspace, "workspace"))) return rc;
+  if (saved_bytes < sl.total)
+    return fail(ALLEGRO_E_INVALID, "saved buffer of %zu bytes is smaller than the %zu required", saved_bytes,
+                sl.total);
+  if (workspace_bytes < wl.total)
+    return fail(ALLEGRO_E_INVALID, "workspace of %zu bytes is smaller than the %zu required", workspace_bytes,
+                wl.total);
+  if (E > 0 && ((rc = check_ptr(h, "h")) || (rc = check_ptr(V, "V")) || (rc = check_ptr(Y, "Y")) ||
+                (rc = check_ptr(dh_out, "dh_out")) || (rc = check_ptr(dV_out, "dV_out")) ||
+                (rc = check_ptr(dh, "dh")) || (rc = check_ptr(dV, "dV")) || (rc = check_ptr(dY, "dY"))))
+    return rc;
+  const DenseTable dn = select_dense(L, H);
+  const MixTable mx = select_mix(plan->lmax, (plan->flags & ALLEGRO_FULL_PARITY) != 0);
+  if (!mx.backward) return fail(ALLEGRO_E_UNSUPPORTED, "no mixing kernel for this plan");
+  void *sv_base = const_cast<void *>(saved);
+  const float *w = at<float>(sv_base, sl.w), *env = at<float>(sv_base, sl.env), *T = at<float>(sv_base, sl.T);
+  const float *sv = at<float>(sv_base, sl.s), *a = at<float>(sv_base, sl.a);
+  float *dT = at<float>(workspace, wl.dT), *da = at<float>(workspace, wl.da), *dhm = at<float>(workspace, wl.dhm);
+  float *ds = at<float>(workspace, wl.ds), *dw = at<float>(workspace, wl.dw), *genv = at<float>(workspace, wl.genv);
+  float *red = at<float>(workspace, wl.red), *mixp = at<float>(workspace, wl.mixp);
+  dn.latent_vjp(s, E, h, sv, a, B1, B2, dh_out, da, dhm, ds, red, dB1, dB2);
+  mx.backward(s, E, dV_out, T, Mix, ds, dT, mixp, dMix);
+  if ((rc = after("allegro_layer_backward"))) return rc;
+  if ((rc = allegro_tp_backward_train(plan, N, E, row_ptr, V, env, W, dT, w, Y, dV, genv, dw, dY, dW,
+                                      at<void>(workspace, wl.tpws), wl.tpws_bytes, stream)))
+    return rc;
+  dn.embed_vjp(s, E, h, A, dw, dhm, red, dA, dh);
+  return after("allegro_layer_backward");
+}
+
+}  // extern "C"

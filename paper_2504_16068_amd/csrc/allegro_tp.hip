@@ -32,9 +32,13 @@
 
 #include "allegro_tp.h"
 #include "cg_builder.hpp"
+#include "device_common.hpp"
+#include "plan.hpp"
 #include "generated/tp_cores.inc"
 
 namespace {
+
+using namespace allegro_dev;
 
 constexpr int kWave = 64;
 
@@ -82,20 +86,6 @@ __device__ __forceinline__ void store_row(float *__restrict__ p, const float (&r
 #pragma unroll
     for (int i = 0; i < D; ++i) p[i] = r[i];
   }
-}
-
-// Streaming 16-byte accesses with the non-temporal hint: x, g, out and grad_x
-// are touched once per kernel, so they should not displace other lines in L2.
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ float4 load_stream(const float4 *p) {
-  const f32x4 v = __builtin_nontemporal_load(reinterpret_cast<const f32x4 *>(p));
-  return make_float4(v.x, v.y, v.z, v.w);
-}
-
-__device__ __forceinline__ void store_stream(float4 v, float4 *p) {
-  const f32x4 w = {v.x, v.y, v.z, v.w};
-  __builtin_nontemporal_store(w, reinterpret_cast<f32x4 *>(p));
 }
 
 // acc + fl(a * b) with two separate roundings (no contraction to FMA).
@@ -160,26 +150,6 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
   }
 #pragma unroll
   for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
-}
-
-// ------------------------------------------------------------ LDS ordering
-// Orders the LDS accesses of the H waves of a workgroup without waiting for
-// their outstanding global memory operations (__syncthreads() also waits for
-// every in-flight global store, which would serialise the tile pipeline).  A
-// single wave executes its LDS operations in order, so for H == 1 only the
-// compiler needs the fences.  No kernel here relies on a barrier for global
-// memory visibility between threads.
-template <int H>
-__device__ __forceinline__ void lds_sync() {
-  if constexpr (H == 1) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  } else {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-  }
 }
 
 // -------------------------------------------------------------------- slabs
@@ -703,30 +673,9 @@ __global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restri
 }
 
 // ------------------------------------------------------------- host side
-thread_local std::string g_last_error;
-
-int fail(int code, const char *fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  std::vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  return code;
-}
+using allegro_internal::fail;
 
 bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
-
-}  // namespace
-
-struct allegro_tp_plan {
-  int lmax = 0, U = 0, flags = 0;
-  allegro::TPTable table;
-  int *status = nullptr;  // device word for ALLEGRO_VALIDATE
-  std::mutex validate_mu;
-};
-
-namespace {
 
 using EnvFn = void (*)(dim3, hipStream_t, int64_t, const int64_t *, const float *, const float *, float *);
 using FwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, float *);
@@ -1052,6 +1001,6 @@ int allegro_sh_backward(const allegro_tp_plan *plan, int64_t E, const double *ve
   return after_launch("allegro_sh_backward");
 }
 
-const char *allegro_last_error(void) { return g_last_error.c_str(); }
+const char *allegro_last_error(void) { return allegro_internal::last_error(); }
 
 }  // extern "C"

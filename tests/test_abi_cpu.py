@@ -17,14 +17,14 @@ from oracle import cg as ocg
 from oracle import irreps as oirreps
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "allegro_tp.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("allegro_tp.h", "allegro_layer.h")]
 
 binding = pytest.importorskip("paper_2504_16068_amd.binding",
                               reason="liballegro_tp.so not built (run __graft_entry__.build())")
 
 
 def _declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(allegro_\w+)\s*\(", text)))
 
@@ -35,6 +35,68 @@ def test_library_exports_every_declared_symbol():
     assert set(names) == set(binding.EXPORTED)
     for name in names:
         assert hasattr(lib, name), name
+
+
+def _declared_arities():
+    """Number of parameters of every function the headers declare."""
+    text = "".join(open(h).read() for h in HEADERS)
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    out = {}
+    for name, params in re.findall(r"\b(allegro_\w+)\s*\(([^;{]*?)\)\s*;", text, flags=re.S):
+        params = params.strip()
+        out[name] = 0 if params in ("", "void") else params.count(",") + 1
+    return out
+
+
+def test_binding_argument_counts_match_headers():
+    lib = binding.library()
+    arities = _declared_arities()
+    assert set(arities) == set(binding.EXPORTED)
+    for name, n in arities.items():
+        fn = getattr(lib, name)
+        if fn.argtypes is not None:
+            assert len(fn.argtypes) == n, (name, len(fn.argtypes), n)
+
+
+def test_layer_rejects_bad_arguments_before_any_launch():
+    lib = binding.library()
+    vp, sz = ctypes.c_void_p, ctypes.c_size_t
+    ok_ptr, ok_rp, bad_ptr = vp(0x10000), vp(0x20000), vp(0x10004)
+    plan = binding.allegro_tp_plan_create(2, 64, binding.ALLEGRO_FULL_PARITY)
+    sv, ws = binding.allegro_layer_buffers(plan, 64, 128, 10, 100)
+    d1, d2, P, U, L, H = plan.d1, plan.d2, plan.n_paths, 64, 64, 128
+    f = 4
+    # saved: w, env, T, s, a; each region rounded up to 256 bytes
+    up = lambda b: (b + 255) // 256 * 256  # noqa: E731
+    assert sv == up(100 * U * f) + up(10 * U * d2 * f) + up(100 * U * d1 * f) + up(100 * U * f) + up(100 * H * f)
+    assert ws > up(100 * U * d1 * f) + binding.allegro_tp_backward_workspace(plan, 10)
+    with pytest.raises(binding.AllegroError) as ex:
+        binding.allegro_layer_buffers(plan, 48, 128, 10, 100)
+    assert ex.value.code == binding.ALLEGRO_E_UNSUPPORTED and "L=48" in str(ex.value)
+    plan32 = binding.allegro_tp_plan_create(2, 32, binding.ALLEGRO_FULL_PARITY)
+    with pytest.raises(binding.AllegroError) as ex:
+        binding.allegro_layer_buffers(plan32, 64, 64, 10, 100)
+    assert ex.value.code == binding.ALLEGRO_E_UNSUPPORTED and "U=64" in str(ex.value)
+    plan32.close()
+    fwd = [plan.handle, L, H, 10, 100, ok_rp] + [ok_ptr] * 10
+    rc, msg = _err(lib.allegro_layer_forward, *fwd, ok_ptr, sz(sv - 1), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "saved" in msg
+    rc, msg = _err(lib.allegro_layer_forward, *fwd, bad_ptr, sz(sv), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "saved" in msg and "aligned" in msg
+    bad = list(fwd)
+    bad[8] = None  # Y
+    rc, msg = _err(lib.allegro_layer_forward, *bad, ok_ptr, sz(sv), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "Y is NULL" in msg
+    rc, msg = _err(lib.allegro_layer_forward, plan.handle, L, H, 0, 5, *([ok_ptr] * 12), sz(sv), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "N=0" in msg
+    bwd = [plan.handle, L, H, 10, 100] + [ok_ptr] * 10
+    rc, msg = _err(lib.allegro_layer_backward, *bwd, sz(sv), *([ok_ptr] * 11), sz(ws - 1), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "workspace" in msg
+    grads = [ok_ptr] * 11
+    grads[5] = None  # dA
+    rc, msg = _err(lib.allegro_layer_backward, *bwd, sz(sv), *grads, sz(ws), None)
+    assert rc == binding.ALLEGRO_E_INVALID and "dA is NULL" in msg
+    plan.close()
 
 
 CONFIGS = [(lmax, full, u) for lmax in (1, 2, 3) for full in (False, True) for u in (16, 32, 64, 128)]
