@@ -15,7 +15,11 @@ Prints ONE JSON line.  The roofline object describes the dominant kernel
 with HIP events on the stream the library launches on.  cpu_baseline times
 the fp64 oracle (single thread) on a prefix of whole center segments.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+The allegro_layer object times one whole Allegro layer (forward, and backward
+with every weight gradient) at the medium model shape of Table I, outside the
+step.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-layer]
        python bench.py --pmc-summary FETCH_CSV WRITE_CSV   (after two rocprofv3 --pmc runs)
 """
 
@@ -62,8 +66,10 @@ def algorithmic_bytes(cfg, n_atoms: int, n_edges: int):
 
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for rel in ("paper_2504_16068_amd/csrc/allegro_tp.hip", "paper_2504_16068_amd/csrc/gen_kernels.cpp",
-                "paper_2504_16068_amd/csrc/cg_builder.cpp"):
+    # every source the tensor-product kernels are compiled from
+    for rel in ("paper_2504_16068_amd/csrc/allegro_tp.hip", "paper_2504_16068_amd/csrc/device_common.hpp",
+                "paper_2504_16068_amd/csrc/gen_kernels.cpp", "paper_2504_16068_amd/csrc/cg_builder.cpp",
+                "paper_2504_16068_amd/csrc/cg_builder.hpp"):
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
@@ -191,6 +197,71 @@ def time_training_backward(torch, at, plan, inputs, grads, per_kernel_ms, reps):
             "workspace_bytes": at.allegro_tp_backward_workspace(plan, rp.numel() - 1)}
 
 
+def layer_algorithmic_bytes(cfg, n_edges: int):
+    """Least bytes one layer must move: every input read once, every output written once.
+
+    forward:  read h [E,L], V [E,U,d1], Y [E,d2]; write h' [E,L], V' [E,U,d1]
+    backward: read h, V, Y, dh' and dV'; write dh, dV, dY
+    (weights, row_ptr and the per-center env are under 0.5% and left out; the
+    activations the forward saves for the backward are an implementation
+    choice and are not counted).
+    """
+    d1, d2, _ = workloads.dims(cfg.lmax, cfg.full_parity)
+    L, UD = cfg.extra["L"], cfg.U * d1
+    fwd = 4 * n_edges * (2 * L + 2 * UD + d2)
+    bwd = 4 * n_edges * (3 * L + 3 * UD + 2 * d2)
+    return {"forward": fwd, "backward": bwd}
+
+
+def time_layer(torch, at, dev, reps, name="medium_layer"):
+    """One Allegro layer (tensor product, mixing, latent MLP, all weight gradients) at the
+    medium model shape: forward and backward timed separately with HIP events."""
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    L, H, e = cfg.extra["L"], cfg.extra["H"], graph.n_edges
+    plan = at.allegro_tp_plan_create(cfg.lmax, cfg.U, at.ALLEGRO_FULL_PARITY if cfg.full_parity else 0)
+    prm = {k: torch.from_numpy(v).to(dev) for k, v in workloads.layer_params(cfg).items()}
+    h, V, dh_out, dV_out = workloads.layer_inputs(cfg, e, dev)
+    rp, y = torch.from_numpy(graph.row_ptr).to(dev), torch.from_numpy(graph.Y).to(dev)
+    sv_b, ws_b = at.allegro_layer_buffers(plan, L, H, graph.n_atoms, e)
+    saved = torch.empty(sv_b, dtype=torch.uint8, device=dev)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
+    h_out, V_out = torch.empty_like(h), torch.empty_like(V)
+    outs = {"h": torch.empty_like(h), "V": torch.empty_like(V), "Y": torch.empty_like(y)}
+    outs.update({k: torch.empty_like(v) for k, v in prm.items()})
+
+    def fwd():
+        at.allegro_layer_forward(plan, L, H, rp, h, V, y, prm, h_out=h_out, V_out=V_out, saved=saved)
+
+    def bwd():
+        at.allegro_layer_backward(plan, L, H, rp, h, V, y, prm, saved, dh_out, dV_out, outs=outs, workspace=ws)
+
+    fwd()
+    bwd()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for k in range(reps):
+        ev[k][0].record()
+        fwd()
+        ev[k][1].record()
+        bwd()
+        ev[k][2].record()
+    torch.cuda.synchronize()
+    f_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(reps)]))
+    b_ms = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(reps)]))
+    algo = layer_algorithmic_bytes(cfg, e)
+    res = {"workload": f"{name}: {graph.n_atoms} atoms, cutoff {cfg.cutoff} A, {e} edges, U={cfg.U}, "
+                       f"lmax={cfg.lmax} full parity, latent L={L}, hidden H={H}",
+           "forward_ms": f_ms, "backward_ms": b_ms, "edges_per_s": e / ((f_ms + b_ms) / 1e3),
+           "algorithmic_bytes": algo,
+           "hbm_algorithmic_GBps": {"forward": algo["forward"] / (f_ms / 1e3) / 1e9,
+                                    "backward": algo["backward"] / (b_ms / 1e3) / 1e9},
+           "saved_bytes": sv_b, "workspace_bytes": ws_b}
+    del saved, ws, h_out, V_out, outs, h, V, dh_out, dV_out
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(graph, host_inputs, max_edges=49152):
     """Time the fp64 oracle (one thread) on a prefix of whole center segments."""
     from threadpoolctl import threadpool_limits
@@ -221,6 +292,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="headline", choices=sorted(workloads.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-layer", action="store_true", help="skip the Allegro layer timing")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the calibrated tp_backward traffic record from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
@@ -331,6 +403,8 @@ def main():
     }
     del x, w, g, out, grads, env
     torch.cuda.empty_cache()
+    if not args.no_layer:
+        result["allegro_layer"] = time_layer(torch, at, dev, max(3, min(args.steps, 10)))
     if not args.no_cpu_baseline:
         cfg_ = cfg
 
