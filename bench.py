@@ -293,6 +293,8 @@ def main():
     ap.add_argument("--workload", default="headline", choices=sorted(workloads.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-layer", action="store_true", help="skip the Allegro layer timing")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="time only the Allegro layer and print its record (no step, no JSON bench line)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the calibrated tp_backward traffic record from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
@@ -309,6 +311,9 @@ def main():
     import paper_2504_16068_amd as at
 
     dev = torch.device("cuda:0")
+    if args.layer_only:
+        print(json.dumps({"allegro_layer": time_layer(torch, at, dev, max(3, min(args.steps, 10)))}), flush=True)
+        return
     graph = workloads.make_graph(args.workload)
     cfg = graph.config
     n_atoms, n_edges = graph.n_atoms, graph.n_edges

@@ -89,29 +89,53 @@ struct RowGemmArgs {
   float *c, *c2;         // output; kEpiSplitAdd: columns < N1 to c, the rest to c2
 };
 
-constexpr int kRowTile = 64;  // rows per workgroup tile; wave w owns rows 16w .. 16w+15
+constexpr int kRowTile = 64;  // rows per workgroup tile
 
+// Stages rows r0 .. r0 + 63 of x [E][KX] into columns col0 .. col0 + KX - 1 of
+// the LDS tile (row stride XS), zero past the last row, with an optional
+// elementwise prologue.  All of a thread's loads are issued before any of its
+// LDS writes, so their latencies overlap.
 template <int KX, int PRO>
 __device__ __forceinline__ void stage_rows(const float *__restrict__ x, int64_t r0, int rows, float *xs, int XS,
                                            int col0, int tid) {
-  for (int f = tid; f < kRowTile * KX / 4; f += kThreads) {
-    const int r = f / (KX / 4), k = 4 * (f % (KX / 4));
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < rows) v = *reinterpret_cast<const float4 *>(x + (r0 + r) * KX + k);
+  constexpr int F4 = kRowTile * KX / 4, PER = (F4 + kThreads - 1) / kThreads;
+  float4 v[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int f = tid + kThreads * i, r = f / (KX / 4), k = 4 * (f % (KX / 4));
+    v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (f < F4 && r < rows) v[i] = *reinterpret_cast<const float4 *>(x + (r0 + r) * KX + k);
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int f = tid + kThreads * i, r = f / (KX / 4), k = 4 * (f % (KX / 4));
+    if (f >= F4) continue;
+    float4 u = v[i];
     if constexpr (PRO == kProSilu) {
-      v.x = silu(v.x); v.y = silu(v.y); v.z = silu(v.z); v.w = silu(v.w);
+      u.x = silu(u.x); u.y = silu(u.y); u.z = silu(u.z); u.w = silu(u.w);
     }
-    *reinterpret_cast<float4 *>(xs + r * XS + col0 + k) = v;
+    *reinterpret_cast<float4 *>(xs + r * XS + col0 + k) = u;
   }
 }
 
+// C[E][N] = X[E][K] B[K][N] over 64-row tiles.  Wave w owns the column tiles
+// w + 4 j of every row tile and keeps their B operands in registers for the
+// whole launch; A operands come from the LDS tile.
 template <int K1, int K2, int N, int N1, int PRO, int EPI>
 __global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
   constexpr int K = K1 + K2, XS = K + 4;  // row stride: the 16 rows of an A read hit distinct banks
-  static_assert(K1 % 16 == 0 && K2 % 16 == 0 && N % 16 == 0 && N1 % 16 == 0, "tile shape");
+  constexpr int NJ = N / 64;              // column tiles per wave
+  static_assert(K1 % 16 == 0 && K2 % 16 == 0 && N % 64 == 0 && N1 % 16 == 0, "tile shape");
   __shared__ float4 xs4[kRowTile * XS / 4];
   float *xs = reinterpret_cast<float *>(xs4);
   const int tid = threadIdx.x, wave = tid / kWave, l = tid % kWave;
+  // step s pairs k = 4 s + l / 16 in both operands
+  float bf[NJ][K / 4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int s = 0; s < K / 4; ++s)
+      bf[j][s] = g.b[(4 * s + l / 16) * g.b_rs + (16 * (wave + 4 * j) + l % 16) * g.b_cs];
   const int64_t n_tiles = (g.E + kRowTile - 1) / kRowTile;
   for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
     const int64_t r0 = t * kRowTile;
@@ -119,29 +143,37 @@ __global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
     stage_rows<K1, PRO>(g.x1, r0, rows, xs, XS, 0, tid);
     if constexpr (K2 > 0) stage_rows<K2, kProNone>(g.x2, r0, rows, xs, XS, K1, tid);
     lds_sync<4>();
-    // step s pairs k = 4 s + l / 16 (with XS = 4 (mod 64) the 64 lanes of an A read hit distinct banks)
-    const float *xa = xs + (16 * wave + l % 16) * XS + l / 16;
 #pragma unroll 1
-    for (int ct = 0; ct < N / 16; ++ct) {
-      const int n = 16 * ct + l % 16;
-      const float *bb = g.b + (l / 16) * g.b_rs + n * g.b_cs;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int rt = 0; rt < kRowTile / 16; ++rt) {
+      // with XS = 4 (mod 64) the 64 lanes of an A read hit distinct banks
+      const float *xa = xs + (16 * rt + l % 16) * XS + l / 16;
+      f32x4 acc[NJ];
 #pragma unroll
-      for (int s = 0; s < K / 4; ++s) acc = mfma_16x16x4(xa[4 * s], bb[4 * s * g.b_rs], acc);
+      for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = 16 * wave + 4 * (l / 16) + r;
-        if (row >= rows) continue;
-        const int64_t e = r0 + row;
-        if constexpr (EPI == kEpiStore) {
-          g.c[e * N + n] = acc[r];
-        } else if constexpr (EPI == kEpiAdd) {
-          g.c[e * N + n] = acc[r] + g.d[e * N + n];
-        } else if constexpr (EPI == kEpiSiluGrad) {
-          g.c[e * N + n] = acc[r] * silu_grad(g.d[e * N + n]);
-        } else {
-          if (16 * ct < N1) g.c[e * N1 + n] = acc[r] + g.d[e * N1 + n];
-          else g.c2[e * (N - N1) + (n - N1)] = acc[r];
+      for (int s = 0; s < K / 4; ++s) {
+        const float a = xa[4 * s];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[j] = mfma_16x16x4(a, bf[j][s], acc[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int ct = wave + 4 * j, n = 16 * ct + l % 16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = 16 * rt + 4 * (l / 16) + r;
+          if (row >= rows) continue;
+          const int64_t e = r0 + row;
+          if constexpr (EPI == kEpiStore) {
+            g.c[e * N + n] = acc[j][r];
+          } else if constexpr (EPI == kEpiAdd) {
+            g.c[e * N + n] = acc[j][r] + g.d[e * N + n];
+          } else if constexpr (EPI == kEpiSiluGrad) {
+            g.c[e * N + n] = acc[j][r] * silu_grad(g.d[e * N + n]);
+          } else {
+            if (16 * ct < N1) g.c[e * N1 + n] = acc[j][r] + g.d[e * N1 + n];
+            else g.c2[e * (N - N1) + (n - N1)] = acc[j][r];
+          }
         }
       }
     }
@@ -227,109 +259,180 @@ __device__ __forceinline__ void component_column(int k, int ne_tile, int &col0, 
   dim = d;
 }
 
-constexpr int kMixEdges = 8;  // edges per tile
-constexpr int kMixCS = kU + 1;  // column stride: 16 consecutive columns hit distinct banks
-constexpr int kChunk = 8;       // float4 per thread in flight while a tile is staged
+constexpr int kMixEdges = 8;       // edges per tile
+constexpr int kMixCS = kU + 1;     // column stride: 16 consecutive columns hit distinct banks
+constexpr int kMixThreads = 512;   // four compute waves, then four memory waves
 
-template <int LMAX, bool FULL, bool BWD>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void mix_kernel(
-    int64_t E, const float *__restrict__ src, const float *__restrict__ mix, const float *__restrict__ ds,
-    float *__restrict__ dst, float *__restrict__ s_out) {
-  using X = XIrreps<LMAX, FULL>;
-  constexpr int U = kU, D1 = X::D1, NX = X::NX, NE = kMixEdges, CS = kMixCS;
-  constexpr int COLS = NE * D1, F4 = NE * U * D1 / 4, PER = (F4 + kThreads - 1) / kThreads;
+// Per-irrep channel mixing, software-pipelined over two LDS tile buffers.
+// Waves 0-3 (compute) hold rows 16w .. 16w+15 of every Mix_c (Mix_c^T for the
+// backward) in registers and run the matrix-core products on one buffer,
+// while waves 4-7 (memory) store the previous tile's results from the other
+// buffer and refill it with the next tile.  Per tile the two roles meet at
+// two workgroup barriers: after the first the compute waves write their
+// results into their buffer in place, after the second the buffers swap.
+// Both roles run the same tile sequence, so their barrier counts match.
+template <class X>
+struct MixTile {
+  static constexpr int U = kU, D1 = X::D1, NX = X::NX, NE = kMixEdges, CS = kMixCS;
+  static constexpr int COLS = NE * D1;
+  static constexpr int BUF = (COLS + 16) * CS;  // +16 columns: the last irrep's padded column tile
+  static constexpr int F4 = NE * U * D1 / 4;    // float4 per full tile
+  static constexpr int PER = (F4 + 255) / 256;  // float4 per memory thread
+  static constexpr int ncols(int c) { return NE * X::dim(c); }
+  static constexpr int nct(int c) { return (ncols(c) + 15) / 16; }
+  static constexpr int ct_off(int c) { return c == 0 ? 0 : ct_off(c - 1) + nct(c - 1); }
+  static constexpr int NCT = ct_off(NX);
   static_assert((U * D1) % 4 == 0, "edge rows must be whole float4");
-  // +16 columns: the last irrep's padded column tile reads past its columns
-  __shared__ float lds[(COLS + 16) * CS];
-  __shared__ int kcol[D1], kdim[D1];
+};
+
+template <class X, bool BWD>
+__device__ __forceinline__ void mix_compute_role(int64_t E, int64_t n_tiles, const float *__restrict__ mix,
+                                                 const float *__restrict__ ds, float *__restrict__ s_out,
+                                                 float *lds) {
+  using M = MixTile<X>;
+  constexpr int U = M::U, CS = M::CS, NE = M::NE;
   const int tid = threadIdx.x, w = tid / kWave, l = tid % kWave;
-  if (tid < D1) component_column<X>(tid, NE, kcol[tid], kdim[tid]);
-  // A operands: wave w's output rows 16w .. 16w+15 of every Mix_c (or Mix_c^T)
-  float A[NX][16];
-  static_for<0, NX>([&](auto ic) {
+  // A operands: row 16 w + l % 16 of Mix_c (or of Mix_c^T), columns 16 (l / 16) + s
+  float A[M::NX][16];
+  static_for<0, M::NX>([&](auto ic) {
     constexpr int c = decltype(ic)::value;
 #pragma unroll
     for (int s = 0; s < 16; ++s)
       A[c][s] = BWD ? mix[(c * U + 16 * (l / 16) + s) * U + 16 * w + l % 16]
                     : mix[(c * U + 16 * w + l % 16) * U + 16 * (l / 16) + s];
   });
-  lds_sync<4>();
-  const int64_t n_tiles = (E + NE - 1) / NE;
-  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+  lds_sync<8>();  // the first tile is in buffer 0
+  int p = 0;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x, ++p) {
+    float *b = lds + (p & 1) * M::BUF;
     const int64_t e0 = t * NE;
     const int ne = int(E - e0 < NE ? E - e0 : NE);
-    const int nf4 = ne * (U * D1 / 4);
-    const float4 *s4 = reinterpret_cast<const float4 *>(src + e0 * U * D1);
-#pragma unroll 1
-    for (int i0 = 0; i0 < PER; i0 += kChunk) {
-      float4 v[kChunk];
+    f32x4 acc[M::NCT];
+    static_for<0, M::NX>([&](auto ic) {
+      constexpr int c = decltype(ic)::value, base = NE * X::off(c);
 #pragma unroll
-      for (int i = 0; i < kChunk; ++i) {
-        const int f = tid + kThreads * (i0 + i);
-        v[i] = f < nf4 ? load_stream(s4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int ct = 0; ct < M::nct(c); ++ct) {
+        const float *bp = b + (base + 16 * ct + l % 16) * CS + 16 * (l / 16);
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 16; ++s) a = mfma_16x16x4(A[c][s], bp[s], a);
+        acc[M::ct_off(c) + ct] = a;
       }
-#pragma unroll
-      for (int i = 0; i < kChunk; ++i) {
-        const int f = tid + kThreads * (i0 + i);
-        if (f >= F4) continue;
-        const float vv[4] = {v[i].x, v[i].y, v[i].z, v[i].w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int idx = 4 * f + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
-          lds[(kcol[k] + e * kdim[k]) * CS + u] = vv[q];
-        }
-      }
-    }
-    lds_sync<4>();
+    });
     if constexpr (!BWD) {
       // s[e][u] = T[e][u][0]: irrep 0 (0e) has one component, so its column is e
-      for (int i = tid; i < ne * U; i += kThreads) s_out[(e0 + i / U) * U + i % U] = lds[(i / U) * CS + i % U];
+      for (int i = tid; i < ne * U; i += 256) s_out[(e0 + i / U) * U + i % U] = b[(i / U) * CS + i % U];
     }
-    static_for<0, NX>([&](auto ic) {
-      constexpr int c = decltype(ic)::value, nq = NE * X::dim(c), NCT = (nq + 15) / 16, base = NE * X::off(c);
-      f32x4 acc[NCT];
+    lds_sync<8>();  // B1: every compute wave has read the tile
+    static_for<0, M::NX>([&](auto ic) {
+      constexpr int c = decltype(ic)::value, base = NE * X::off(c), nq = M::ncols(c);
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const float *bp = lds + (base + 16 * ct + l % 16) * CS + 16 * (l / 16);
-        acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 16; ++s) acc[ct] = mfma_16x16x4(A[c][s], bp[s], acc[ct]);
-      }
-      lds_sync<4>();  // every wave has read irrep c's columns
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
+      for (int ct = 0; ct < M::nct(c); ++ct) {
         const int q = 16 * ct + l % 16;
         if (q >= nq) continue;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int uo = 16 * w + 4 * (l / 16) + r;
-          float val = acc[ct][r];
+          float val = acc[M::ct_off(c) + ct][r];
           if constexpr (BWD && c == 0) {
             if (q < ne) val += ds[(e0 + q) * U + uo];
           }
-          lds[(base + q) * CS + uo] = val;
+          b[(base + q) * CS + uo] = val;
         }
       }
     });
-    lds_sync<4>();
-    float4 *d4 = reinterpret_cast<float4 *>(dst + e0 * U * D1);
-#pragma unroll 1
-    for (int i0 = 0; i0 < PER; i0 += kChunk) {
-#pragma unroll
-      for (int i = 0; i < kChunk; ++i) {
-        const int f = tid + kThreads * (i0 + i);
-        if (f >= nf4) continue;
-        float vv[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int idx = 4 * f + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
-          vv[q] = lds[(kcol[k] + e * kdim[k]) * CS + u];
-        }
-        store_stream(make_float4(vv[0], vv[1], vv[2], vv[3]), d4 + f);
-      }
-    }
-    lds_sync<4>();
+    lds_sync<8>();  // B2: results are in the buffer
   }
+}
+
+template <class X>
+__device__ __forceinline__ void mix_memory_role(int64_t E, int64_t n_tiles, const float *__restrict__ src,
+                                                float *__restrict__ dst, float *lds) {
+  using M = MixTile<X>;
+  constexpr int U = M::U, D1 = M::D1, NE = M::NE, PER = M::PER, F4 = M::F4;
+  const int mt = int(threadIdx.x) - 256;
+  // LDS offset (within a buffer) of each of the thread's elements: component k
+  // of channel u of edge e sits in column NE off(c) + e dim(c) + m, row u
+  int addr[PER][4];
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = 4 * (mt + 256 * i) + q;
+      int a = 0;
+      if (idx < 4 * F4) {
+        const int e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
+        int col0, dim;
+        component_column<X>(k, NE, col0, dim);
+        a = (col0 + e * dim) * M::CS + u;
+      }
+      addr[i][q] = a;
+    }
+  auto count = [&](int64_t t) { return int(E - t * NE < NE ? E - t * NE : NE) * (U * D1 / 4); };
+  auto load = [&](int64_t t, float4 (&v)[PER]) {
+    const int nf4 = count(t);
+    const float4 *s4 = reinterpret_cast<const float4 *>(src + t * NE * U * D1);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = mt + 256 * i;
+      v[i] = f < nf4 ? load_stream(s4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto put = [&](float *b, const float4 (&v)[PER]) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (mt + 256 * i >= F4) continue;
+      b[addr[i][0]] = v[i].x;
+      b[addr[i][1]] = v[i].y;
+      b[addr[i][2]] = v[i].z;
+      b[addr[i][3]] = v[i].w;
+    }
+  };
+  auto store = [&](int64_t t, const float *b) {
+    const int nf4 = count(t);
+    float4 *d4 = reinterpret_cast<float4 *>(dst + t * NE * U * D1);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = mt + 256 * i;
+      if (f < nf4) store_stream(make_float4(b[addr[i][0]], b[addr[i][1]], b[addr[i][2]], b[addr[i][3]]), d4 + f);
+    }
+  };
+  // The tile after the next one is loaded into registers one period ahead,
+  // so its loads stay in flight across the barriers and the compute waves'
+  // write-back.
+  const int64_t G = gridDim.x;
+  int64_t t = blockIdx.x;
+  float4 v[PER];
+  if (t < n_tiles) {
+    load(t, v);
+    put(lds, v);
+  }
+  if (t + G < n_tiles) load(t + G, v);
+  lds_sync<8>();
+  int p = 0;
+  for (; t < n_tiles; t += G, ++p) {
+    // each LDS element is read (store of tile t - G) and then overwritten (tile
+    // t + G) by the same thread, so program order alone orders the two
+    float *b = lds + ((p + 1) & 1) * M::BUF;
+    if (p > 0) store(t - G, b);
+    if (t + G < n_tiles) put(b, v);
+    if (t + 2 * G < n_tiles) load(t + 2 * G, v);
+    lds_sync<8>();  // B1
+    lds_sync<8>();  // B2: the compute waves have written tile t's results
+  }
+  if (p > 0) store(t - G, lds + ((p + 1) & 1) * M::BUF);
+}
+
+template <int LMAX, bool FULL, bool BWD>
+__global__ __launch_bounds__(kMixThreads) void mix_kernel(int64_t E, const float *__restrict__ src,
+                                                          const float *__restrict__ mix,
+                                                          const float *__restrict__ ds, float *__restrict__ dst,
+                                                          float *__restrict__ s_out) {
+  using X = XIrreps<LMAX, FULL>;
+  __shared__ float lds[2 * MixTile<X>::BUF];
+  const int64_t n_tiles = (E + kMixEdges - 1) / kMixEdges;
+  if (threadIdx.x < 256) mix_compute_role<X, BWD>(E, n_tiles, mix, ds, s_out, lds);
+  else mix_memory_role<X>(E, n_tiles, src, dst, lds);
 }
 
 constexpr int kWgEdges = 4;        // edges per tile: column counts NE * (2l + 1) are multiples of 4
@@ -468,7 +571,17 @@ int after(const char *what) {
   return ALLEGRO_OK;
 }
 
-unsigned row_grid(int64_t E) { return unsigned(std::min<int64_t>(cdiv(E, kRowTile), 8192)); }
+// Workgroups of `kernel` (static LDS only) that the device holds at once; at
+// least one per compute unit.
+int64_t resident_groups(const void *kernel, int threads) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu <= 0)
+    per_cu = 1;
+  return int64_t(cus) * per_cu;
+}
 
 void colsum(hipStream_t s, int64_t R, int C, const float *part, float *out) {
   hipLaunchKernelGGL(colsum_kernel, dim3(unsigned(cdiv(C, 256))), dim3(256), 0, s, int(R), C, part, out);
@@ -478,10 +591,14 @@ void colsum(hipStream_t s, int64_t R, int C, const float *part, float *out) {
 template <int L, int H>
 struct DenseOps {
   static constexpr int U = kU;
+  // one workgroup per slot the GPU holds at once: each loads its B operands once
   template <int K1, int K2, int N, int N1, int PRO, int EPI>
   static void row(hipStream_t s, const RowGemmArgs &g) {
     if (g.E == 0) return;
-    hipLaunchKernelGGL((row_gemm_kernel<K1, K2, N, N1, PRO, EPI>), dim3(row_grid(g.E)), dim3(kThreads), 0, s, g);
+    static const int64_t slots =
+        resident_groups(reinterpret_cast<const void *>(&row_gemm_kernel<K1, K2, N, N1, PRO, EPI>), kThreads);
+    const unsigned G = unsigned(std::min<int64_t>(cdiv(g.E, kRowTile), slots));
+    hipLaunchKernelGGL((row_gemm_kernel<K1, K2, N, N1, PRO, EPI>), dim3(G), dim3(kThreads), 0, s, g);
   }
   template <int M1, int M2, int N, int PRO>
   static void reduce(hipStream_t s, int64_t E, const float *p1, const float *p2, const float *q, float *part,
@@ -546,20 +663,25 @@ DenseTable select_dense(int L, int H) {
 // Launchers of the mixing kernels of one (lmax, parity).
 template <int LMAX, bool FULL>
 struct MixOps {
+  // one workgroup per tile slot the GPU holds at once: each streams a fixed tile sequence
+  template <bool BWD>
+  static unsigned grid(int64_t E) {
+    static const int64_t slots = resident_groups(reinterpret_cast<const void *>(&mix_kernel<LMAX, FULL, BWD>),
+                                                 kMixThreads);
+    return unsigned(std::min<int64_t>(cdiv(E, kMixEdges), slots));
+  }
   static void forward(hipStream_t s, int64_t E, const float *T, const float *mix, float *V_out, float *sv) {
     if (E == 0) return;
-    const unsigned G = unsigned(std::min<int64_t>(cdiv(E, kMixEdges), kMaxPersistent));
-    hipLaunchKernelGGL((mix_kernel<LMAX, FULL, false>), dim3(G), dim3(kThreads), 0, s, E, T, mix, nullptr, V_out,
-                       sv);
+    hipLaunchKernelGGL((mix_kernel<LMAX, FULL, false>), dim3(grid<false>(E)), dim3(kMixThreads), 0, s, E, T, mix,
+                       nullptr, V_out, sv);
   }
   static void backward(hipStream_t s, int64_t E, const float *dV_out, const float *T, const float *mix,
                        const float *ds, float *dT, float *part, float *dmix) {
     using X = XIrreps<LMAX, FULL>;
     const int64_t Gw = wgrad_groups(E);
     if (E > 0) {
-      const unsigned G = unsigned(std::min<int64_t>(cdiv(E, kMixEdges), kMaxPersistent));
-      hipLaunchKernelGGL((mix_kernel<LMAX, FULL, true>), dim3(G), dim3(kThreads), 0, s, E, dV_out, mix, ds, dT,
-                         nullptr);
+      hipLaunchKernelGGL((mix_kernel<LMAX, FULL, true>), dim3(grid<true>(E)), dim3(kMixThreads), 0, s, E, dV_out,
+                         mix, ds, dT, nullptr);
       hipLaunchKernelGGL((mix_wgrad_kernel<LMAX, FULL>), dim3(unsigned(Gw)), dim3(kThreads), 0, s, E, dV_out, T,
                          part);
     }
