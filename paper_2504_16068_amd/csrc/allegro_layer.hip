@@ -260,7 +260,10 @@ __device__ __forceinline__ void component_column(int k, int ne_tile, int &col0, 
 }
 
 constexpr int kMixEdges = 8;       // edges per tile
-constexpr int kMixCS = kU + 1;     // column stride: 16 consecutive columns hit distinct banks
+// Column stride (floats): a multiple of 4, so a lane reads its 16 B operands
+// of a step block as four 16-byte LDS loads, and 68 = 4 (mod 64), so the 16
+// columns of a tile start in distinct bank quads.
+constexpr int kMixCS = kU + 4;
 constexpr int kMixThreads = 512;   // four compute waves, then four memory waves
 
 // Per-irrep channel mixing, software-pipelined over two LDS tile buffers.
@@ -283,6 +286,7 @@ struct MixTile {
   static constexpr int ct_off(int c) { return c == 0 ? 0 : ct_off(c - 1) + nct(c - 1); }
   static constexpr int NCT = ct_off(NX);
   static_assert((U * D1) % 4 == 0, "edge rows must be whole float4");
+  static_assert(CS % 4 == 0, "operand blocks are read as 16-byte LDS loads");
 };
 
 template <class X, bool BWD>
@@ -312,10 +316,17 @@ __device__ __forceinline__ void mix_compute_role(int64_t E, int64_t n_tiles, con
       constexpr int c = decltype(ic)::value, base = NE * X::off(c);
 #pragma unroll
       for (int ct = 0; ct < M::nct(c); ++ct) {
-        const float *bp = b + (base + 16 * ct + l % 16) * CS + 16 * (l / 16);
+        // the lane's 16 operands (channels 16 (l / 16) .. + 15 of column 16 ct + l % 16) are contiguous
+        const float4 *bp = reinterpret_cast<const float4 *>(b + (base + 16 * ct + l % 16) * CS + 16 * (l / 16));
+        float bv[16];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 x = bp[j];
+          bv[4 * j] = x.x; bv[4 * j + 1] = x.y; bv[4 * j + 2] = x.z; bv[4 * j + 3] = x.w;
+        }
         f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int s = 0; s < 16; ++s) a = mfma_16x16x4(A[c][s], bp[s], a);
+        for (int s = 0; s < 16; ++s) a = mfma_16x16x4(A[c][s], bv[s], a);
         acc[M::ct_off(c) + ct] = a;
       }
     });
