@@ -255,3 +255,51 @@ def test_layer_medium_full_size(at, n_samples=12, n_ranges=4):
     lay, ref = _oracle(cfg.lmax, cfg.full_parity, L, H, graph.row_ptr[:c1 + 1], host[0], host[1], graph.Y[:t], prm,
                        host[2], host[3])
     _compare(lay, (_np(hr), _np(Vr), _host(gr)), ref, f"medium_layer[first {c1} centers, {t} edges]")
+
+
+def test_layer_replays_in_a_hip_graph(at):
+    """Forward and backward of one layer captured once into a HIP graph and replayed
+    several times, with eager work and synchronisation between replays; every replay
+    must equal the eager result bit for bit."""
+    graph = workloads.make_graph("layer_small")
+    cfg = graph.config
+    L, H = cfg.extra["L"], cfg.extra["H"]
+    _note("[gpu] HIP graph replay of one layer, layer_small")
+    plan = _plan(at, cfg.lmax, cfg.full_parity)
+    prm = {k: _t(v) for k, v in workloads.layer_params(cfg).items()}
+    h, V, dh_out, dV_out = (_t(a) for a in workloads.layer_inputs(cfg, graph.n_edges))
+    rp, Y = _t(graph.row_ptr), _t(graph.Y)
+    sv, ws = at.allegro_layer_buffers(plan, L, H, graph.n_atoms, graph.n_edges)
+    saved = torch.empty(sv, dtype=torch.uint8, device=DEV)
+    work = torch.empty(ws, dtype=torch.uint8, device=DEV)
+    h_out, V_out = torch.empty_like(h), torch.empty_like(V)
+    outs = {"h": torch.empty_like(h), "V": torch.empty_like(V), "Y": torch.empty_like(Y)}
+    outs.update({k: torch.empty_like(v) for k, v in prm.items()})
+
+    def step():
+        at.allegro_layer_forward(plan, L, H, rp, h, V, Y, prm, h_out=h_out, V_out=V_out, saved=saved)
+        at.allegro_layer_backward(plan, L, H, rp, h, V, Y, prm, saved, dh_out, dV_out, outs=outs, workspace=work)
+
+    results = [h_out, V_out] + [outs[k] for k in sorted(outs)]
+    step()
+    torch.cuda.synchronize()
+    eager = [r.clone() for r in results]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    hip_graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(hip_graph):
+        step()
+    for rep in range(3):
+        for r in results:
+            r.fill_(float("nan"))  # eager work between replays
+        saved.fill_(0xFF)
+        work.fill_(0xFF)
+        torch.cuda.synchronize()
+        hip_graph.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(results, eager):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), rep
