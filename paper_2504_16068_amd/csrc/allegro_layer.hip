@@ -58,14 +58,6 @@ __device__ __forceinline__ float silu_grad(float a) {
   return sg * (1.0f + a * (1.0f - sg));
 }
 
-template <int C, int END, class F>
-__device__ __forceinline__ void static_for(F &&f) {
-  if constexpr (C < END) {
-    f(std::integral_constant<int, C>{});
-    static_for<C + 1, END>(f);
-  }
-}
-
 // The x irreps of a plan: for l = 0..lmax, (l, natural parity) then, with
 // full parity, (l, the other parity); sizes 2l + 1, concatenated.
 template <int LMAX, bool FULL>

@@ -297,63 +297,78 @@ struct KernelTraits {
   static constexpr int bwd_occupancy(bool wg) { return wg ? 2 : kBwdOccupancy; }
 };
 
-// ------------------------------------------------------ tensor product fwd
+// Waves per center.  A center's slabs are dealt round robin to NW waves of
+// one workgroup (with two channel halves, U = 128, the first NW/2 waves take
+// half 0 and the rest half 1); each wave streams its slabs through its own
+// LDS tile.  With many waves on one center the concurrently streamed HBM
+// regions are few and contiguous: a standalone probe of the forward's access
+// pattern measured 4.98 TB/s with one wave per center and 5.51 TB/s with 16.
+// That pays where the kernel is HBM-bound (lmax <= 2, and the lmax-3
+// backward at 128 channels).  Where it is bound by VALU issue (lmax 3 at 64
+// channels, and the forward at lmax 3), fewer waves per center leave room
+// for more workgroups per compute unit, which overlap one center's reduction
+// phases with another's streaming.  The counts are the fastest of 1, 2, 4, 8
+// (16) measured for each kernel on the MI355X.
 template <class Core, int U>
-__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kFwdOccupancy))) void tp_forward_kernel(const int64_t *__restrict__ row_ptr,
+struct TPWaves {
+  static constexpr bool kHigh = Core::LMAX >= 3, kWide = U > 64;
+  static constexpr int kFwd = kHigh ? 2 : 16;
+  static constexpr int bwd(bool wg) { return wg ? (kHigh && !kWide ? 2 : 4) : (kHigh && !kWide ? 4 : 8); }
+};
+
+// ------------------------------------------------------ tensor product fwd
+template <class Core, int U, int NW = TPWaves<Core, U>::kFwd>
+__global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::kFwdOccupancy))) void tp_forward_kernel(const int64_t *__restrict__ row_ptr,
                                                            const float *__restrict__ x,
                                                            const float *__restrict__ env,
                                                            const float *__restrict__ path_w,
                                                            float *__restrict__ out) {
   using L = Lanes<U>;
-  constexpr int D1 = Core::D1, D2 = Core::D2;
-  constexpr int T = U > kWave ? 1 : (36 / D1 > 1 ? 36 / D1 : 1);  // slabs per tile (about 9 KB of LDS)
-  constexpr int TF4 = T * TileShape<D1>::SF4;
-  __shared__ float4 tile[TF4];
+  constexpr int D1 = Core::D1, D2 = Core::D2, WPT = NW / L::CPL;
+  constexpr int TF4 = TileShape<D1>::SF4;  // one slab per tile
+  static_assert(NW % L::CPL == 0, "waves split evenly over the channel halves");
+  __shared__ float4 tiles[NW * TF4];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, ul = lane % L::LPE;
+  const int t = wave / WPT, first = wave % WPT;
+  float4 *tile = tiles + wave * TF4;
   float *tile_f = reinterpret_cast<float *>(tile);
-  const int lane = threadIdx.x, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
   const int64_t n_slabs = Slabs<U>::count(e1 - e0);
-#pragma unroll 1
-  for (int t = 0; t < L::CPL; ++t) {
-    const int u = ul + t * kWave;
-    RegWeights<Core::NP> wr;
-    wr.load(path_w, U, u);
-    float er[D2];
-    load_row<D2>(env + (n * U + u) * D2, er);
-    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
-      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
-      tile_load<U, D1, TF4>(x, tile, e0, e1, s0, cnt, t, lane);
-      lds_sync<1>();
-#pragma unroll 1
-      for (int s = 0; s < cnt; ++s) {
-        if (row_valid<U>(e0, e1, s0 + s, lane)) {
-          float *row = tile_f + (s * kWave + lane) * D1;
-          float xr[D1], orow[D1];
+  const int u = ul + t * kWave;
+  RegWeights<Core::NP> wr;
+  wr.load(path_w, U, u);
+  float er[D2];
+  load_row<D2>(env + (n * U + u) * D2, er);
+  for (int64_t s = first; s < n_slabs; s += WPT) {
+    tile_load<U, D1, TF4>(x, tile, e0, e1, s, 1, t, lane);
+    lds_sync<1>();
+    if (row_valid<U>(e0, e1, s, lane)) {
+      float *row = tile_f + lane * D1;
+      float xr[D1], orow[D1];
 #pragma unroll
-          for (int i = 0; i < D1; ++i) xr[i] = row[i];
-          Core::fwd(xr, er, wr, orow);
+      for (int i = 0; i < D1; ++i) xr[i] = row[i];
+      Core::fwd(xr, er, wr, orow);
 #pragma unroll
-          for (int i = 0; i < D1; ++i) row[i] = orow[i];
-        }
-      }
-      lds_sync<1>();
-      tile_store<U, D1, TF4>(out, tile, e0, e1, s0, cnt, t, lane);
-      lds_sync<1>();
+      for (int i = 0; i < D1; ++i) row[i] = orow[i];
     }
+    lds_sync<1>();
+    tile_store<U, D1, TF4>(out, tile, e0, e1, s, 1, t, lane);
+    lds_sync<1>();
   }
 }
 
 // ------------------------------------------------------ tensor product bwd
-// Pass 1 over channel half t: grad_x rows in place in the x tile, this lane's
-// grad_env partial sums in ge and, with WG, its path-weight gradient sums in sw.
-template <class Core, int U, int T, int TF4, bool WG>
+// Pass 1 of one wave: for its slabs of channel half t, grad_x rows in place in
+// its x tile, this lane's grad_env partial sums in ge and, with WG, its
+// path-weight gradient sums in sw.
+template <class Core, int U, bool WG>
 __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const float *__restrict__ g,
                                           const float *__restrict__ env, const float *__restrict__ path_w,
                                           float *__restrict__ grad_x, float4 *tile_x, float4 *tile_g, int64_t n,
-                                          int64_t e0, int64_t e1, int64_t n_slabs, int t, int lane,
-                                          float (&ge)[Core::D2], float (&sw)[Core::NP]) {
-  constexpr int D1 = Core::D1, D2 = Core::D2;
+                                          int64_t e0, int64_t e1, int64_t n_slabs, int64_t first, int64_t step,
+                                          int t, int lane, float (&ge)[Core::D2], float (&sw)[Core::NP]) {
+  constexpr int D1 = Core::D1, D2 = Core::D2, TF4 = TileShape<D1>::SF4;
   const int u = lane % Lanes<U>::LPE + t * kWave;
   constexpr bool kCached = KernelTraits<Core>::cached_weights(WG);
   typename std::conditional<kCached, CachedWeights, RegWeights<Core::NP>>::type wr;
@@ -364,138 +379,140 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
   for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
   float *tx = reinterpret_cast<float *>(tile_x);
   const float *tg = reinterpret_cast<const float *>(tile_g);
-  for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
-    const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
-    tile_load<U, D1, TF4>(x, tile_x, e0, e1, s0, cnt, t, lane);
-    tile_load<U, D1, TF4>(g, tile_g, e0, e1, s0, cnt, t, lane);
+  for (int64_t s = first; s < n_slabs; s += step) {
+    tile_load<U, D1, TF4>(x, tile_x, e0, e1, s, 1, t, lane);
+    tile_load<U, D1, TF4>(g, tile_g, e0, e1, s, 1, t, lane);
     lds_sync<1>();
-#pragma unroll 1
-    for (int s = 0; s < cnt; ++s) {
-      if (row_valid<U>(e0, e1, s0 + s, lane)) {
-        // x row in, grad_x row out, in place in the LDS tile
-        float *row = tx + (s * kWave + lane) * D1;
-        const float *grow = tg + (s * kWave + lane) * D1;
-        if constexpr (kCached) wr.renew();
-        if constexpr (WG) Core::wgrad(row, er, grow, sw);
-        Core::bwd(row, er, wr, grow, row, ge);
-      }
+    if (row_valid<U>(e0, e1, s, lane)) {
+      // x row in, grad_x row out, in place in the LDS tile
+      float *row = tx + lane * D1;
+      const float *grow = tg + lane * D1;
+      if constexpr (kCached) wr.renew();
+      if constexpr (WG) Core::wgrad(row, er, grow, sw);
+      Core::bwd(row, er, wr, grow, row, ge);
     }
     lds_sync<1>();
-    tile_store<U, D1, TF4>(grad_x, tile_x, e0, e1, s0, cnt, t, lane);
+    tile_store<U, D1, TF4>(grad_x, tile_x, e0, e1, s, 1, t, lane);
     lds_sync<1>();
   }
 }
 
+// LDS layout of the backward (floats), reused by its phases:
+//   pass 1:    NW pairs of x and g tiles;
+//   path-weight partial sums: [NW][64][PC] for a chunk of PC paths (WG only);
+//   grad_env:  partial sums [NW][64][D2], then grad_env[n] [U][D2], then each
+//              wave's staged w and Y rows of pass 2 [NW][EB][U + 1 + D2].
+template <class Core, int U, bool WG, int NW_>
+struct BwdLds {
+  static constexpr int NW = NW_, D2 = Core::D2, NP = Core::NP;
+  static constexpr int TILE_F4 = TileShape<Core::D1>::SF4;
+  static constexpr int EB = 8;          // edges per pass-2 batch of one wave (8 lanes per edge)
+  static constexpr int WROW = U + 1;    // padded w row: per-lane row reads hit distinct banks
+  static constexpr int P1 = NW * 2 * TILE_F4 * 4;
+  static constexpr int GE_PART = NW * kWave * D2;
+  static constexpr int GE_ROW = U * D2;
+  static constexpr int STAGE = EB * (WROW + D2);
+  static constexpr int P2 = GE_PART + GE_ROW + NW * STAGE;
+  static constexpr int PC_FIT = P1 / (NW * kWave);
+  static constexpr int PC = WG ? (NP < PC_FIT ? NP : PC_FIT) : 1;  // paths per reduction chunk
+  static constexpr int SW = WG ? NW * kWave * PC : 0;
+  static constexpr int FLOATS = P1 > P2 ? (P1 > SW ? P1 : SW) : (P2 > SW ? P2 : SW);
+  static_assert(!WG || PC >= 1, "LDS too small for the path-weight partial sums");
+};
+
 // With WG the kernel also writes center n's path-weight gradient, summed over
 // its edges, to pw_part[n][p][u] (the first of the two reduction stages).
-template <class Core, int U, bool WG>
-__global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::bwd_occupancy(WG)))) void tp_backward_kernel(
+template <class Core, int U, bool WG, int NW = TPWaves<Core, U>::bwd(WG)>
+__global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(KernelTraits<Core>::bwd_occupancy(WG)))) void tp_backward_kernel(
         const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
         const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
         const float *__restrict__ Y, float *__restrict__ grad_x, float *__restrict__ grad_env,
         float *__restrict__ grad_w, float *__restrict__ grad_Y, float *__restrict__ pw_part) {
   using L = Lanes<U>;
-  constexpr int D1 = Core::D1, D2 = Core::D2;
-  constexpr int T = U > kWave ? 1 : (18 / D1 > 1 ? 18 / D1 : 1);  // slabs per tile (two tiles: x and g)
-  constexpr int TILE_F4 = T * TileShape<D1>::SF4;
-  // One LDS buffer serves both passes: the x and g tiles in pass 1; in pass 2
-  // grad_env[n] of all channels followed by staged w and Y rows (at least
-  // kMinBatch edges) or by the lane groups' partial sums.
-  constexpr int WROW = U + 1;  // padded w row: per-lane row reads hit distinct banks
-  constexpr int kMinBatch = 8;
-  constexpr int P1_FLOATS = 2 * TILE_F4 * 4;
-  constexpr int PART_FLOATS = L::G > 1 ? kWave * D2 : 0;
-  constexpr int ROWS_FLOATS = kMinBatch * (WROW + D2);
-  constexpr int P2_FLOATS = U * D2 + (PART_FLOATS > ROWS_FLOATS ? PART_FLOATS : ROWS_FLOATS);
-  constexpr int SMEM_FLOATS = P1_FLOATS > P2_FLOATS ? P1_FLOATS : P2_FLOATS;
-  __shared__ float4 smem[(SMEM_FLOATS + 3) / 4];
-  float4 *tile_x = smem, *tile_g = smem + TILE_F4;
-  float *ge_l = reinterpret_cast<float *>(smem);  // pass 2: grad_env[n, :, :]
-  float *rest = ge_l + U * D2;                    // partial sums, then pass-2 w / Y rows
-  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  using B = BwdLds<Core, U, WG, NW>;
+  constexpr int D2 = Core::D2, NP = Core::NP, WPT = NW / L::CPL, NT = NW * kWave;
+  static_assert(NW % L::CPL == 0, "waves split evenly over the channel halves");
+  __shared__ float4 smem[(B::FLOATS + 3) / 4];
+  float *lds = reinterpret_cast<float *>(smem);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int t = wave / WPT;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
   const int64_t n_slabs = Slabs<U>::count(e1 - e0);
 
-  // Pass 1 (lane <-> channel): grad_x per edge, grad_env accumulated in registers.
-#pragma unroll 1
-  for (int t = 0; t < L::CPL; ++t) {
-    const int u = ul + t * kWave;
-    float ge[D2], sw[Core::NP];
-    if constexpr (WG) {
+  // Pass 1 (lane <-> channel): grad_x per edge, partial sums per wave in registers.
+  float ge[D2], sw[NP];
+  if constexpr (WG) {
 #pragma unroll
-      for (int p = 0; p < Core::NP; ++p) sw[p] = 0.0f;
-    }
-    bwd_pass1<Core, U, T, TILE_F4, WG>(x, g, env, path_w, grad_x, tile_x, tile_g, n, e0, e1, n_slabs, t, lane, ge,
-                                       sw);
-    if constexpr (WG) {
-      // lane groups hold the same channel: butterfly sums in a fixed order (the
-      // two operands of each step are swapped between partner lanes, so every
-      // lane of a channel ends with the same bits)
-#pragma unroll
-      for (int p = 0; p < Core::NP; ++p) {
-#pragma unroll
-        for (int off = L::LPE; off < kWave; off *= 2) sw[p] += __shfl_xor(sw[p], off);
-      }
-      if (grp == 0) {
-#pragma unroll
-        for (int p = 0; p < Core::NP; ++p) pw_part[(n * Core::NP + p) * U + u] = sw[p];
-      }
-    }
-    // grad_env of this channel half goes straight to its output
-    if constexpr (L::G == 1) {
-      store_row<D2>(grad_env + (n * U + u) * D2, ge);
-    } else {
-      // combine the lane groups in a fixed order (the tile loop is done with the buffer)
-#pragma unroll
-      for (int j = 0; j < D2; ++j) rest[lane * D2 + j] = ge[j];
-      lds_sync<1>();
-      if (grp == 0) {
-        float acc[D2];
-#pragma unroll
-        for (int j = 0; j < D2; ++j) {
-          acc[j] = rest[ul * D2 + j];
-          for (int q = 1; q < L::G; ++q) acc[j] += rest[(q * L::LPE + ul) * D2 + j];
-        }
-        store_row<D2>(grad_env + (n * U + u) * D2, acc);
-      }
-    }
+    for (int p = 0; p < NP; ++p) sw[p] = 0.0f;
   }
-  lds_sync<1>();
-  // Stage grad_env[n] in LDS for pass 2.  Every lane copies back only values it
-  // stored itself, so program order alone makes them visible to it.
-  if (grp == 0) {
-#pragma unroll
-    for (int t = 0; t < L::CPL; ++t) {
-      float v[D2];
-      load_row<D2>(grad_env + (n * U + ul + t * kWave) * D2, v);
-#pragma unroll
-      for (int j = 0; j < D2; ++j) ge_l[(ul + t * kWave) * D2 + j] = v[j];
-    }
-  }
-  lds_sync<1>();
+  float4 *tile_x = smem + wave * 2 * B::TILE_F4, *tile_g = tile_x + B::TILE_F4;
+  bwd_pass1<Core, U, WG>(x, g, env, path_w, grad_x, tile_x, tile_g, n, e0, e1, n_slabs, wave % WPT, WPT, t, lane,
+                         ge, sw);
+  lds_sync<NW>();  // every wave is done with its tiles
 
-  // Pass 2: the embedding's VJP through grad_env, in batches of EB edges whose w and
-  // Y rows are first staged into the (now free) tile memory with one round of
-  // coalesced loads:
+  if constexpr (WG) {
+    // lane groups hold the same channel: butterfly sums in a fixed order (the
+    // two operands of each step are swapped between partner lanes, so every
+    // lane of a channel ends with the same bits)
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+#pragma unroll
+      for (int off = L::LPE; off < kWave; off *= 2) sw[p] += __shfl_xor(sw[p], off);
+    }
+    // then over the waves of the channel half, in wave order, PC paths at a time
+    static_for<0, (NP + B::PC - 1) / B::PC>([&](auto ic) {
+      constexpr int p0 = decltype(ic)::value * B::PC, pn = NP - p0 < B::PC ? NP - p0 : B::PC;
+      if (grp == 0) {
+#pragma unroll
+        for (int q = 0; q < pn; ++q) lds[(wave * kWave + ul) * B::PC + q] = sw[p0 + q];
+      }
+      lds_sync<NW>();
+      for (int i = tid; i < U * pn; i += NT) {
+        const int q = i / U, uu = i % U, tt = uu / kWave, uw = uu % L::LPE;
+        float a = 0.0f;
+        for (int k = 0; k < WPT; ++k) a += lds[((tt * WPT + k) * kWave + uw) * B::PC + q];
+        pw_part[(n * NP + p0 + q) * U + uu] = a;
+      }
+      lds_sync<NW>();
+    });
+  }
+
+  // grad_env: the waves' and lane groups' partial sums, in a fixed order
+  float *ge_part = lds, *ge_l = lds + B::GE_PART;
+#pragma unroll
+  for (int j = 0; j < D2; ++j) ge_part[(wave * kWave + lane) * D2 + j] = ge[j];
+  lds_sync<NW>();
+  for (int i = tid; i < U * D2; i += NT) {
+    const int uu = i / D2, j = i % D2, tt = uu / kWave, uw = uu % L::LPE;
+    float a = 0.0f;
+    for (int k = 0; k < WPT; ++k)
+      for (int q = 0; q < L::G; ++q) a += ge_part[((tt * WPT + k) * kWave + q * L::LPE + uw) * D2 + j];
+    ge_l[i] = a;
+    grad_env[n * U * D2 + i] = a;
+  }
+  lds_sync<NW>();
+
+  // Pass 2: the embedding's VJP through grad_env, in batches of EB edges dealt
+  // round robin to the waves; each wave first stages the batch's w and Y rows
+  // in its own LDS area with one round of coalesced loads:
   //   grad_w[e,u] = sum_j grad_env[n,u,j] Y[e,j]   lane <-> channel (coalesced stores)
-  //   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> edge; grad_env from LDS
-  //                                                as wave-uniform broadcasts
-  // w rows are padded to U+1 floats so the per-lane row reads hit distinct banks.
-  constexpr int ROOM = SMEM_FLOATS - U * D2;
-  constexpr int EB = ROOM / (WROW + D2) < kWave ? ROOM / (WROW + D2) : kWave;
-  static_assert(EB >= kMinBatch, "LDS buffer too small for a batch of w rows");
-  float *wl = rest;
+  //   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> (edge k, channel eighth q):
+  //                 each lane sums U/8 channels, then an xor butterfly over the 8
+  //                 lanes of the edge (operands swapped between partners, so all 8
+  //                 hold the same bits)
+  constexpr int EB = B::EB, WROW = B::WROW;
+  float *wl = lds + B::GE_PART + B::GE_ROW + wave * B::STAGE;
   float *yl = wl + EB * WROW;
   const float4 *w4 = reinterpret_cast<const float4 *>(w);
   float gel[L::CPL][D2];
 #pragma unroll
-  for (int t = 0; t < L::CPL; ++t)
+  for (int c = 0; c < L::CPL; ++c)
 #pragma unroll
-    for (int j = 0; j < D2; ++j) gel[t][j] = ge_l[(ul + t * kWave) * D2 + j];
-  for (int64_t eb = e0; eb < e1; eb += EB) {
+    for (int j = 0; j < D2; ++j) gel[c][j] = ge_l[(ul + c * kWave) * D2 + j];
+  for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
-    lds_sync<1>();  // the previous batch is done with the staged rows
+    lds_sync<1>();  // this wave's previous batch is done with its staged rows
     for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
       const float4 v = w4[eb * (U / 4) + i4];
       const int r = (4 * i4) / U, c = (4 * i4) % U;
@@ -506,25 +523,34 @@ __global__ __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(KernelTra
     lds_sync<1>();
     for (int k = grp; k < cnt; k += L::G) {
 #pragma unroll
-      for (int t = 0; t < L::CPL; ++t) {
+      for (int c = 0; c < L::CPL; ++c) {
         float acc = 0.0f;
 #pragma unroll
-        for (int j = 0; j < D2; ++j) acc = __builtin_fmaf(gel[t][j], yl[k * D2 + j], acc);
-        grad_w[(eb + k) * U + ul + t * kWave] = acc;
+        for (int j = 0; j < D2; ++j) acc = __builtin_fmaf(gel[c][j], yl[k * D2 + j], acc);
+        grad_w[(eb + k) * U + ul + c * kWave] = acc;
       }
     }
-    if (lane < cnt) {
-      const float *wrow = wl + lane * WROW;
+    {
+      constexpr int UQ = U / 8;  // channels per lane
+      const int k = lane / 8, q = lane % 8;
+      const float *wrow = wl + k * WROW + q * UQ;
+      const float *gq = ge_l + q * UQ * D2;
       float gy[D2];
 #pragma unroll
       for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
+      if (k < cnt) {
 #pragma unroll 4
-      for (int u = 0; u < U; ++u) {
-        const float wv = wrow[u];
+        for (int uu = 0; uu < UQ; ++uu) {
+          const float wv = wrow[uu];
 #pragma unroll
-        for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(ge_l[u * D2 + j], wv, gy[j]);
+          for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(gq[uu * D2 + j], wv, gy[j]);
+        }
       }
-      store_row<D2>(grad_Y + (eb + lane) * D2, gy);
+#pragma unroll
+      for (int off = 1; off < 8; off *= 2)
+#pragma unroll
+        for (int j = 0; j < D2; ++j) gy[j] += __shfl_xor(gy[j], off);
+      if (k < cnt && q == 0) store_row<D2>(grad_Y + (eb + k) * D2, gy);
     }
   }
 }
@@ -690,15 +716,16 @@ void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const fl
 template <class Core, int U>
 void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 float *out) {
-  hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave), 0, s, rp, x, env, pw, out);
+  hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave * TPWaves<Core, U>::kFwd), 0, s, rp, x, env, pw,
+                     out);
 }
 
 template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
                 float *pw_part) {
-  hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave), 0, s, rp, x, env, pw, g, w, Y, gx, genv,
-                     gw, gy, pw_part);
+  hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x, env, pw,
+                     g, w, Y, gx, genv, gw, gy, pw_part);
 }
 
 struct Kernels {

@@ -3,6 +3,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 namespace allegro_dev {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -35,6 +37,16 @@ __device__ __forceinline__ void lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  }
+}
+
+// Calls f(std::integral_constant<int, C>{}) for C = BEGIN .. END - 1, so that
+// the body can index register arrays with compile-time constants.
+template <int BEGIN, int END, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (BEGIN < END) {
+    f(std::integral_constant<int, BEGIN>{});
+    static_for<BEGIN + 1, END>(f);
   }
 }
 

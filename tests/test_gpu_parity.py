@@ -334,10 +334,16 @@ def test_train_backward_parity(at, case):
     env = at.allegro_env_embed(plan, rp, wd, yd)
     base = at.allegro_tp_backward(plan, rp, xd, env, pwd, gd, wd, yd)
     (gx, genv, gw, gy, gpw), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
-    # the other gradients are those of the inference backward, bit for bit
-    for a, b in zip((gx, genv, gw, gy), base):
-        assert _same_bits(a, b)
+    # grad_x is per edge: bit for bit that of the inference backward; the segment
+    # sums (grad_env and through it grad_w, grad_Y) split the edges over a
+    # different number of waves, so they agree to fp32 rounding, and both match
+    # the oracle
+    assert _same_bits(gx, base[0])
     t = otp.TensorProduct(lmax, full)
+    renv = otp.env_embed(data[0], data[2], data[3])
+    ref = t.backward(data[0], data[1], renv, data[4], data[5], data[2], data[3])
+    for got, r, blocks in zip((genv, gw, gy), ref[1:], (t.env_slices, None, t.env_slices)):
+        assert block_rel_err(got.cpu().numpy(), r, blocks) <= BWD_TOL
     ref = t.path_weight_grad(data[0], data[1], otp.env_embed(data[0], data[2], data[3]), data[5])
     err = block_rel_err(gpw.cpu().numpy(), ref)
     _note(f"training backward {case}: grad_path_w err={err:.2e}")
