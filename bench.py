@@ -104,8 +104,9 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
     copy_kib = (4 << 30) / 1024
 
     def per_launch(rows, kernel):
-        # the inference backward only (template flag false), not the training variant
-        pat = re.compile(kernel + r"<.*,\s*false>")
+        # the inference backward only (template flag false, then the waves per
+        # center), not the training variant
+        pat = re.compile(kernel + r"<.*,\s*false(,\s*\d+)?>")
         vals = [float(r["Counter_Value"]) for r in rows if pat.search(r["Kernel_Name"])]
         return sum(vals) / len(vals), len(vals)
 
