@@ -227,13 +227,35 @@ __global__ __launch_bounds__(kThreads) void reduce_gemm_kernel(int64_t E, const 
         out[(16 * mt + 4 * (l / 16) + r) * N + 16 * (wave + 4 * j) + l % 16] = acc[mt][j][r];
 }
 
+// out[c] = sum over r of part[r][c], in a fixed order: a block owns 16
+// columns; thread (g, c) sums rows g, g + 16, g + 32, ... with four
+// accumulators, then the 16 row groups are added in order.
+constexpr int kColsumCols = 16, kColsumGroups = 16;
+
 __global__ __launch_bounds__(256) void colsum_kernel(int R, int C, const float *__restrict__ part,
                                                      float *__restrict__ out) {
-  const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
-  if (c >= C) return;
-  float a = 0.0f;
-  for (int r = 0; r < R; ++r) a += part[int64_t(r) * C + c];
-  out[c] = a;
+  __shared__ float sums[kColsumGroups][kColsumCols];
+  const int cl = int(threadIdx.x) % kColsumCols, g = int(threadIdx.x) / kColsumCols;
+  const int c = int(blockIdx.x) * kColsumCols + cl;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  if (c < C) {
+    int r = g;
+    constexpr int S = kColsumGroups;
+    for (; r + 3 * S < R; r += 4 * S) {
+      a0 += part[int64_t(r) * C + c];
+      a1 += part[int64_t(r + S) * C + c];
+      a2 += part[int64_t(r + 2 * S) * C + c];
+      a3 += part[int64_t(r + 3 * S) * C + c];
+    }
+    for (; r < R; r += S) a0 += part[int64_t(r) * C + c];
+  }
+  sums[g][cl] = (a0 + a1) + (a2 + a3);
+  __syncthreads();
+  if (g == 0 && c < C) {
+    float a = sums[0][cl];
+    for (int k = 1; k < kColsumGroups; ++k) a += sums[k][cl];
+    out[c] = a;
+  }
 }
 
 // ------------------------------------------------------------ mixing
@@ -587,7 +609,7 @@ int64_t resident_groups(const void *kernel, int threads) {
 }
 
 void colsum(hipStream_t s, int64_t R, int C, const float *part, float *out) {
-  hipLaunchKernelGGL(colsum_kernel, dim3(unsigned(cdiv(C, 256))), dim3(256), 0, s, int(R), C, part, out);
+  hipLaunchKernelGGL(colsum_kernel, dim3(unsigned(cdiv(C, kColsumCols))), dim3(256), 0, s, int(R), C, part, out);
 }
 
 // Launchers of the dense contractions of a layer with latent width L and hidden width H.

@@ -308,12 +308,12 @@ struct KernelTraits {
 // channels, and the forward at lmax 3), fewer waves per center leave room
 // for more workgroups per compute unit, which overlap one center's reduction
 // phases with another's streaming.  The counts are the fastest of 1, 2, 4, 8
-// (16) measured for each kernel on the MI355X.
+// and 16 measured for each kernel on the MI355X.
 template <class Core, int U>
 struct TPWaves {
   static constexpr bool kHigh = Core::LMAX >= 3, kWide = U > 64;
   static constexpr int kFwd = kHigh ? 2 : 16;
-  static constexpr int bwd(bool wg) { return wg ? (kHigh && !kWide ? 2 : 4) : (kHigh && !kWide ? 4 : 8); }
+  static constexpr int bwd(bool wg) { return wg ? (kHigh && !kWide ? 2 : 4) : (kHigh ? (kWide ? 8 : 4) : 16); }
 };
 
 // ------------------------------------------------------ tensor product fwd
