@@ -325,6 +325,15 @@ __device__ __forceinline__ void mix_compute_role(int64_t E, int64_t n_tiles, con
     float *b = lds + (p & 1) * M::BUF;
     const int64_t e0 = t * NE;
     const int ne = int(E - e0 < NE ? E - e0 : NE);
+    // backward: the lane's ds terms for the 0e columns (column q = edge q), loaded
+    // now so that their latency hides under the products
+    float dsv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (BWD) {
+      if (l % 16 < ne) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dsv[r] = ds[(e0 + l % 16) * U + 16 * w + 4 * (l / 16) + r];
+      }
+    }
     f32x4 acc[M::NCT];
     static_for<0, M::NX>([&](auto ic) {
       constexpr int c = decltype(ic)::value, base = NE * X::off(c);
@@ -359,9 +368,7 @@ __device__ __forceinline__ void mix_compute_role(int64_t E, int64_t n_tiles, con
         for (int r = 0; r < 4; ++r) {
           const int uo = 16 * w + 4 * (l / 16) + r;
           float val = acc[M::ct_off(c) + ct][r];
-          if constexpr (BWD && c == 0) {
-            if (q < ne) val += ds[(e0 + q) * U + uo];
-          }
+          if constexpr (BWD && c == 0) val += dsv[r];  // zero for columns past the tile's edges
           b[(base + q) * CS + uo] = val;
         }
       }
