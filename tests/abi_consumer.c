@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include "allegro_layer.h"
 #include "allegro_tp.h"
 
 #define CHECK(cond, ...)                  \
@@ -64,6 +65,31 @@ int main(void) {
     free(val);
     CHECK(allegro_tp_plan_destroy(plan) == ALLEGRO_OK, "destroy");
     printf("ok lmax=%d full=%d d1=%d d2=%d paths=%d nnz=%d\n", lmax, full, d1, d2, np, nnz);
+  }
+  /* the layer's buffer sizes are host arithmetic; its shape checks run before any GPU call */
+  {
+    allegro_tp_plan *plan = NULL;
+    CHECK(allegro_tp_plan_create(&plan, 3, 64, ALLEGRO_FULL_PARITY) == ALLEGRO_OK, "layer plan");
+    size_t saved = 0, work = 0;
+    CHECK(allegro_layer_buffers(plan, 64, 128, 100, 5000, &saved, &work) == ALLEGRO_OK, "layer buffers");
+    /* saved holds at least w [E][U], env [N][U][d2], T [E][U][d1], s [E][U] and a [E][H] */
+    const size_t floats = (size_t)5000 * 64 + (size_t)100 * 64 * 16 + (size_t)5000 * 64 * 32 + (size_t)5000 * 64 +
+                          (size_t)5000 * 128;
+    CHECK(saved >= floats * sizeof(float) && saved < floats * sizeof(float) + 5 * 256, "saved bytes %zu", saved);
+    CHECK(work > (size_t)5000 * 64 * 32 * sizeof(float), "workspace bytes %zu", work);
+    CHECK(allegro_layer_buffers(plan, 48, 128, 100, 5000, &saved, &work) == ALLEGRO_E_UNSUPPORTED, "L=48");
+    CHECK(allegro_layer_forward(plan, 64, 128, 0, 5, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL,
+                                NULL, NULL, 0, NULL) == ALLEGRO_E_INVALID,
+          "layer E>0 with N=0");
+    CHECK(allegro_layer_forward(plan, 64, 128, 0, 0, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL,
+                                NULL, NULL, 0, NULL) == ALLEGRO_OK,
+          "layer empty no-op");
+    CHECK(allegro_tp_plan_destroy(plan) == ALLEGRO_OK, "destroy");
+    allegro_tp_plan *narrow = NULL;
+    CHECK(allegro_tp_plan_create(&narrow, 2, 32, ALLEGRO_FULL_PARITY) == ALLEGRO_OK, "U=32 plan");
+    CHECK(allegro_layer_buffers(narrow, 64, 64, 10, 10, &saved, &work) == ALLEGRO_E_UNSUPPORTED, "layer U=32");
+    CHECK(allegro_tp_plan_destroy(narrow) == ALLEGRO_OK, "destroy");
+    printf("ok layer\n");
   }
   allegro_tp_plan *bad = (allegro_tp_plan *)1;
   CHECK(allegro_tp_plan_create(&bad, 4, 64, 0) == ALLEGRO_E_UNSUPPORTED && bad == NULL, "lmax 4 rejected");

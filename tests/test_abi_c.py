@@ -2,7 +2,8 @@
 
 Host-only calls: plan sizes for every (lmax, parity), the selection rules of
 the reported paths, the orthonormality of the reported coupling coefficients,
-the workspace size and early error returns.
+the workspace size, the layer's buffer sizes and shape checks, and early
+error returns.
 """
 
 import os
@@ -27,4 +28,4 @@ def test_c_consumer(tmp_path):
     env["LD_LIBRARY_PATH"] = "/opt/rocm/lib:" + env.get("LD_LIBRARY_PATH", "")
     res = subprocess.run([str(exe)], capture_output=True, text=True, env=env, timeout=120)
     assert res.returncode == 0, res.stdout + res.stderr
-    assert res.stdout.count("ok lmax=") == 6 and "ok errors" in res.stdout
+    assert res.stdout.count("ok lmax=") == 6 and "ok layer" in res.stdout and "ok errors" in res.stdout
