@@ -469,54 +469,39 @@ __global__ __launch_bounds__(kMixThreads) void mix_kernel(int64_t E, const float
 
 constexpr int kWgEdges = 4;        // edges per tile: column counts NE * (2l + 1) are multiples of 4
 constexpr int kWgCS = kU + 16;     // = 16 (mod 64): the four lane groups of an operand read hit distinct banks
+constexpr int kWgThreads = 512;    // four compute waves, then four memory waves
 
-template <int LMAX, bool FULL>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void mix_wgrad_kernel(
-    int64_t E, const float *__restrict__ dv, const float *__restrict__ tt, float *__restrict__ part) {
-  using X = XIrreps<LMAX, FULL>;
-  constexpr int U = kU, D1 = X::D1, NX = X::NX, NE = kWgEdges, CS = kWgCS;
-  constexpr int COLS = NE * D1, F4 = NE * U * D1 / 4, PER = (F4 + kThreads - 1) / kThreads;
+// dMix_c = sum over edges and components of dV'_c T_c^T, software-pipelined
+// over two LDS buffers that each hold a tile of dV' and of T in the column
+// layout of the mixing kernel.  Waves 0-3 (compute) own rows 16w .. 16w+15 of
+// every dMix_c as register accumulators; waves 4-7 (memory) keep the next tile
+// in registers and move it into the free buffer while the compute waves work
+// on the other.  One barrier per tile; both roles run the same tile sequence.
+// Each workgroup writes one partial of every dMix_c.
+template <class X>
+struct WgTile {
+  static constexpr int U = kU, D1 = X::D1, NE = kWgEdges, CS = kWgCS;
+  static constexpr int COLS = NE * D1;
+  static constexpr int BUF = 2 * COLS * CS;     // dV' then T
+  static constexpr int F4 = NE * U * D1 / 4;    // float4 per tensor and tile
+  static constexpr int PER = (F4 + 255) / 256;  // float4 per memory thread and tensor
   static_assert((U * D1) % 4 == 0, "edge rows must be whole float4");
-  __shared__ float la[COLS * CS], lb[COLS * CS];
+};
+
+template <class X>
+__device__ __forceinline__ void wgrad_compute_role(int64_t n_tiles, float *lds, float *__restrict__ part) {
+  using M = WgTile<X>;
+  constexpr int U = M::U, CS = M::CS, NE = M::NE, NX = X::NX;
   const int tid = threadIdx.x, w = tid / kWave, l = tid % kWave;
-  // every tile puts the thread's elements at the same LDS addresses
-  int addr[PER][4];
-#pragma unroll
-  for (int i = 0; i < PER; ++i)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int idx = 4 * (tid + kThreads * i) + q, e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1,
-                k = rem % D1;
-      int col0, dim;
-      component_column<X>(k, NE, col0, dim);
-      addr[i][q] = (col0 + e * dim) * CS + u;
-    }
   f32x4 acc[NX][4];
 #pragma unroll
   for (int c = 0; c < NX; ++c)
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) acc[c][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int64_t n_tiles = (E + NE - 1) / NE;
-  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
-    const int64_t e0 = t * NE;
-    const int ne = int(E - e0 < NE ? E - e0 : NE);
-    const int nf4 = ne * (U * D1 / 4);
-    const float4 *a4 = reinterpret_cast<const float4 *>(dv + e0 * U * D1);
-    const float4 *b4 = reinterpret_cast<const float4 *>(tt + e0 * U * D1);
-    float4 va[PER], vb[PER];
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int f = tid + kThreads * i;
-      va[i] = f < nf4 ? load_stream(a4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
-      vb[i] = f < nf4 ? load_stream(b4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (tid + kThreads * i >= F4) continue;
-      la[addr[i][0]] = va[i].x; la[addr[i][1]] = va[i].y; la[addr[i][2]] = va[i].z; la[addr[i][3]] = va[i].w;
-      lb[addr[i][0]] = vb[i].x; lb[addr[i][1]] = vb[i].y; lb[addr[i][2]] = vb[i].z; lb[addr[i][3]] = vb[i].w;
-    }
-    lds_sync<4>();
+  lds_sync<8>();  // the first tile is in buffer 0
+  int p = 0;
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x, ++p) {
+    const float *la = lds + (p & 1) * M::BUF, *lb = la + M::COLS * CS;
     // dMix_c[v][u] += sum_q dV'_c[q][v] T_c[q][u]; lane group l / 16 owns
     // the quarter of the irrep's columns q = (l / 16) * nq / 4 + s
     static_for<0, NX>([&](auto ic) {
@@ -529,7 +514,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int nt = 0; nt < 4; ++nt) acc[c][nt] = mfma_16x16x4(a, lb[(q0 + s) * CS + 16 * nt + l % 16], acc[c][nt]);
       }
     });
-    lds_sync<4>();
+    lds_sync<8>();  // this buffer is free again; the other holds the next tile
   }
   float *out = part + int64_t(blockIdx.x) * NX * U * U;
 #pragma unroll
@@ -539,6 +524,77 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         out[(c * U + 16 * w + 4 * (l / 16) + r) * U + 16 * nt + l % 16] = acc[c][nt][r];
+}
+
+template <class X>
+__device__ __forceinline__ void wgrad_memory_role(int64_t E, int64_t n_tiles, const float *__restrict__ dv,
+                                                  const float *__restrict__ tt, float *lds) {
+  using M = WgTile<X>;
+  constexpr int U = M::U, D1 = M::D1, NE = M::NE, PER = M::PER, F4 = M::F4;
+  const int mt = int(threadIdx.x) - 256;
+  // LDS offset (within a tensor's tile) of each of the thread's elements
+  int addr[PER][4];
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = 4 * (mt + 256 * i) + q;
+      int a = 0;
+      if (idx < 4 * F4) {
+        const int e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
+        int col0, dim;
+        component_column<X>(k, NE, col0, dim);
+        a = (col0 + e * dim) * M::CS + u;
+      }
+      addr[i][q] = a;
+    }
+  float4 va[PER], vb[PER];
+  auto load = [&](int64_t t) {
+    const int nf4 = int(E - t * NE < NE ? E - t * NE : NE) * (U * D1 / 4);
+    const float4 *a4 = reinterpret_cast<const float4 *>(dv + t * NE * U * D1);
+    const float4 *b4 = reinterpret_cast<const float4 *>(tt + t * NE * U * D1);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = mt + 256 * i;
+      va[i] = f < nf4 ? load_stream(a4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+      vb[i] = f < nf4 ? load_stream(b4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto put = [&](float *b) {
+    float *la = b, *lb = b + M::COLS * M::CS;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (mt + 256 * i >= F4) continue;
+      la[addr[i][0]] = va[i].x; la[addr[i][1]] = va[i].y; la[addr[i][2]] = va[i].z; la[addr[i][3]] = va[i].w;
+      lb[addr[i][0]] = vb[i].x; lb[addr[i][1]] = vb[i].y; lb[addr[i][2]] = vb[i].z; lb[addr[i][3]] = vb[i].w;
+    }
+  };
+  const int64_t G = gridDim.x;
+  int64_t t = blockIdx.x;
+  if (t < n_tiles) {
+    load(t);
+    put(lds);
+  }
+  if (t + G < n_tiles) load(t + G);
+  lds_sync<8>();
+  for (int p = 0; t < n_tiles; t += G, ++p) {
+    // the compute waves read buffer p & 1; fill the other with tile t + G, then
+    // start the loads of tile t + 2G
+    if (t + G < n_tiles) put(lds + ((p + 1) & 1) * M::BUF);
+    if (t + 2 * G < n_tiles) load(t + 2 * G);
+    lds_sync<8>();
+  }
+}
+
+template <int LMAX, bool FULL>
+__global__ __launch_bounds__(kWgThreads) void mix_wgrad_kernel(int64_t E, const float *__restrict__ dv,
+                                                               const float *__restrict__ tt,
+                                                               float *__restrict__ part) {
+  using X = XIrreps<LMAX, FULL>;
+  __shared__ float lds[2 * WgTile<X>::BUF];
+  const int64_t n_tiles = (E + kWgEdges - 1) / kWgEdges;
+  if (threadIdx.x < 256) wgrad_compute_role<X>(n_tiles, lds, part);
+  else wgrad_memory_role<X>(E, n_tiles, dv, tt, lds);
 }
 
 // ------------------------------------------------------------- host side
@@ -710,11 +766,14 @@ struct MixOps {
   static void backward(hipStream_t s, int64_t E, const float *dV_out, const float *T, const float *mix,
                        const float *ds, float *dT, float *part, float *dmix) {
     using X = XIrreps<LMAX, FULL>;
-    const int64_t Gw = wgrad_groups(E);
+    // resident workgroups (one per compute unit), at most the partials the workspace holds
+    static const int64_t slots = std::min<int64_t>(
+        resident_groups(reinterpret_cast<const void *>(&mix_wgrad_kernel<LMAX, FULL>), kWgThreads), kMaxPersistent);
+    const int64_t Gw = std::min<int64_t>(wgrad_groups(E), slots);
     if (E > 0) {
       hipLaunchKernelGGL((mix_kernel<LMAX, FULL, true>), dim3(grid<true>(E)), dim3(kMixThreads), 0, s, E, dV_out,
                          mix, ds, dT, nullptr);
-      hipLaunchKernelGGL((mix_wgrad_kernel<LMAX, FULL>), dim3(unsigned(Gw)), dim3(kThreads), 0, s, E, dV_out, T,
+      hipLaunchKernelGGL((mix_wgrad_kernel<LMAX, FULL>), dim3(unsigned(Gw)), dim3(kWgThreads), 0, s, E, dV_out, T,
                          part);
     }
     colsum(s, Gw, X::NX * kU * kU, part, dmix);
