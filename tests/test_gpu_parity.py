@@ -174,6 +174,60 @@ def test_edge_cases(at, lmax, full, U, degrees):
     assert np.all(env[np.asarray(degrees) == 0] == 0)
 
 
+@pytest.mark.parametrize("lmax,full,U", [(2, True, 64), (3, True, 128), (1, False, 16)])
+def test_skewed_degrees(at, lmax, full, U):
+    """Heavy-tailed segment lengths: many empty centers, many short ones, a few with
+    hundreds of edges and one with thousands, so that every wave of a center's
+    workgroup gets many slabs, few or none.
+
+    A segment sum over n edges in fp32 carries a rounding error that grows with n,
+    so at thousands of edges the relative bars (set for the workloads' ~50
+    neighbours) do not apply to env itself.  What is exact or bounded is checked:
+    the deterministic env equals the fp32 sequential replay bit for bit; the fast
+    env is within the recursive-summation bound gamma_n * sum |w Y| of the fp64
+    sum (one rounding per step with FMA, u = 2^-24); and the forward, inference
+    backward and training backward, fed the deterministic env, match the oracle
+    evaluated on that same env at the usual bars."""
+    rng = np.random.default_rng(1000 + lmax * 10 + U)
+    degrees = np.floor(rng.pareto(1.2, size=160) * 6).astype(np.int64)
+    degrees[rng.choice(160, 40, replace=False)] = 0
+    degrees[7] = 3001 if U <= 64 else 1200
+    degrees = np.minimum(degrees, 3001)
+    _note(f"[gpu] skewed degrees lmax={lmax} U={U}: E={int(degrees.sum())}, max={int(degrees.max())}, "
+          f"empty={int((degrees == 0).sum())}")
+    row_ptr, x, w, y, pw, g = _synthetic(lmax, full, U, degrees, seed=5 + lmax + U)
+    rp, xd, wd, yd, pwd, gd = (_t(a) for a in (row_ptr, x, w, y, pw, g))
+    # env: deterministic mode bit-exact, fast mode within the summation bound
+    det = at.allegro_env_embed(_plan(at, lmax, U, full, det=True), rp, wd, yd)
+    env32 = otp.env_embed_fp32_replay(row_ptr, w, y)
+    assert np.array_equal(det.cpu().numpy().view(np.uint32), env32.view(np.uint32))
+    plan = _plan(at, lmax, U, full)
+    fast = at.allegro_env_embed(plan, rp, wd, yd).cpu().numpy().astype(np.float64)
+    abs_sum = otp.env_embed(row_ptr, np.abs(w), np.abs(y))
+    n_seg = np.diff(row_ptr).astype(np.float64)[:, None, None]
+    gamma = n_seg * 2.0 ** -24 / (1 - n_seg * 2.0 ** -24)
+    assert np.all(np.abs(fast - otp.env_embed(row_ptr, w, y)) <= gamma * abs_sum + 1e-30)
+    # the rest on the deterministic env, against the oracle on the same env values
+    out = at.allegro_tp_forward(plan, rp, xd, det, pwd)
+    grads = at.allegro_tp_backward(plan, rp, xd, det, pwd, gd, wd, yd)
+    (gx, genv, gw, gy, gpw), _ = _train(at, plan, rp, xd, det, pwd, gd, wd, yd)
+    t = otp.TensorProduct(lmax, full)
+    ref_out = t.forward(row_ptr, x, env32, pw)
+    ref_g = t.backward(row_ptr, x, env32, pw, g, w, y)
+    errs = {"out": block_rel_err(out.cpu().numpy(), ref_out, t.x_slices)}
+    for name, got, ref, blocks in (("grad_x", grads[0], ref_g[0], t.x_slices),
+                                   ("grad_env", grads[1], ref_g[1], t.env_slices),
+                                   ("grad_w", grads[2], ref_g[2], None), ("grad_Y", grads[3], ref_g[3], t.env_slices),
+                                   ("train grad_env", genv, ref_g[1], t.env_slices),
+                                   ("train grad_Y", gy, ref_g[3], t.env_slices)):
+        errs[name] = block_rel_err(got.cpu().numpy(), ref, blocks)
+    errs["grad_path_w"] = block_rel_err(gpw.cpu().numpy(), t.path_weight_grad(row_ptr, x, env32, g))
+    _note(f"skewed lmax{lmax} U{U}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    assert errs["out"] <= FWD_TOL
+    assert all(v <= BWD_TOL for k, v in errs.items() if k != "out"), errs
+    assert _same_bits(gx, grads[0])
+
+
 def test_no_edges_gives_zero_env_and_grad_env(at):
     _note("[gpu] E = 0 with N = 4")
     plan = _plan(at, 2, 64, True)
