@@ -358,6 +358,116 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   }
 }
 
+// ------------------------------------------ tensor product fwd, lmax 3
+// The forward as a per-center matrix (generated TPMFwd): out = M x with
+// M[k][i] = sum_{p = (a(i), b, c(k))} W(p) sum_j C_pijk env[j], built once per
+// center and channel.  M has about 900 entries per channel at lmax 3, too
+// many for one lane, so its rows are split over the NW waves of the center's
+// workgroup: every wave reads every row of x and writes ROWS components of
+// out.  Tiles of T slabs are staged through LDS rows padded to D1 + 4 floats
+// (16-byte row reads by 16 consecutive lanes hit distinct bank quads); every
+// thread holds its share of the next tile in registers, so one tile of loads
+// is in flight while the current one is computed.  Per edge and channel this
+// takes about 900 FMAs instead of about 2,000 instructions, which makes the
+// lmax-3 forward HBM-bound.
+template <class Core>
+constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
+
+template <class Core, int U>
+__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_forward_m_kernel(
+    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+    const float *__restrict__ path_w, float *__restrict__ out) {
+  using MF = TPMFwd<Core::LMAX, Core::FULL>;
+  using L = Lanes<U>;
+  constexpr int D1 = Core::D1, D2 = Core::D2, NW = MF::NW, ROWS = MF::ROWS;
+  constexpr int T = U > kWave ? 4 : 8;      // slabs per tile (32 or 64 KB; 8 at U = 128 would spill)
+  constexpr int RS = D1 + 4;                // padded LDS row stride (floats)
+  constexpr int R4 = D1 / 4;                // float4 per row
+  constexpr int SF4 = TileShape<D1>::SF4;   // float4 per slab
+  constexpr int TF4 = T * SF4;              // float4 per tile
+  constexpr int NT = NW * kWave;
+  constexpr int PER = (TF4 + NT - 1) / NT;  // float4 per thread and tile
+  static_assert(D1 % 4 == 0 && D1 == NW * ROWS, "rows of whole float4, split evenly over the waves");
+  __shared__ float4 xs4[T * kWave * RS / 4], os4[T * kWave * RS / 4];
+  float *xs = reinterpret_cast<float *>(xs4), *os = reinterpret_cast<float *>(os4);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int64_t n = blockIdx.x;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
+  // float4 f of a tile starting at slab s0: its HBM index, or -1 past the segment
+  auto src = [&](int64_t s0, int f, int t) -> int64_t {
+    const int sl = f / SF4, in = f % SF4;
+    if (s0 + sl >= n_slabs) return -1;
+    if constexpr (U <= kWave) {
+      const int64_t base = Slabs<U>::first_edge(e0, s0) * (U * D1 / 4), end = e1 * (U * D1 / 4);
+      const int64_t g = base + f;
+      return g < end ? g : -1;
+    } else {
+      return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
+    }
+  };
+#pragma unroll 1
+  for (int t = 0; t < L::CPL; ++t) {
+    const int u = lane % L::LPE + t * kWave;
+    float4 v[PER];
+    auto fetch = [&](int64_t s0) {
+      const float4 *x4 = reinterpret_cast<const float4 *>(x);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int f = tid + NT * i;
+        const int64_t g = f < TF4 ? src(s0, f, t) : -1;
+        v[i] = g >= 0 ? load_stream(x4 + g) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    };
+    // M first: its weight loads would otherwise wait behind the tile's loads
+    // (one in-order counter covers both)
+    float m[MF::MAXM];
+    {
+      CachedWeights wr;
+      wr.load(path_w, U, u);
+      float er[D2];
+      load_row<D2>(env + (n * U + u) * D2, er);
+      MF::build(wave, er, wr, m);
+    }
+    if (n_slabs > 0) fetch(0);
+    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+      // the tile from registers into LDS (padded rows), then the next tile's loads
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int f = tid + NT * i;
+        if (f < TF4) *reinterpret_cast<float4 *>(xs + (f / R4) * RS + 4 * (f % R4)) = v[i];
+      }
+      if (s0 + T < n_slabs) fetch(s0 + T);
+      lds_sync<NW>();
+      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+#pragma unroll 1
+      for (int sl = 0; sl < cnt; ++sl) {
+        const int r = sl * kWave + lane;
+        float xr[D1], o[ROWS];
+#pragma unroll
+        for (int q = 0; q < R4; ++q) {
+          const float4 a = *reinterpret_cast<const float4 *>(xs + r * RS + 4 * q);
+          xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
+        }
+        MF::apply(wave, xr, m, o);
+#pragma unroll
+        for (int k = 0; k < ROWS; ++k) os[r * RS + wave * ROWS + k] = o[k];
+      }
+      lds_sync<NW>();
+      float4 *o4 = reinterpret_cast<float4 *>(out);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int f = tid + NT * i;
+        const int64_t g = f < TF4 ? src(s0, f, t) : -1;
+        if (g >= 0) store_stream(*reinterpret_cast<const float4 *>(os + (f / R4) * RS + 4 * (f % R4)), o4 + g);
+      }
+      // the next iteration writes xs (read above, before the barrier) and then os
+      // only after its own barrier, by which every thread has read os here
+    }
+    lds_sync<NW>();  // both tiles are free before the next channel half
+  }
+}
+
 // ------------------------------------------------------ tensor product bwd
 // Pass 1 of one wave: for its slabs of channel half t, grad_x rows in place in
 // its x tile, this lane's grad_env partial sums in ge and, with WG, its
@@ -716,8 +826,11 @@ void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const fl
 template <class Core, int U>
 void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 float *out) {
-  hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave * TPWaves<Core, U>::kFwd), 0, s, rp, x, env, pw,
-                     out);
+  if constexpr (Core::LMAX >= 3)
+    hipLaunchKernelGGL((tp_forward_m_kernel<Core, U>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, out);
+  else
+    hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave * TPWaves<Core, U>::kFwd), 0, s, rp, x, env, pw,
+                       out);
 }
 
 template <class Core, int U, bool WG>

@@ -18,6 +18,7 @@
 // W is any accessor with W(p) = the lane's weight of path p.
 //
 // Usage: gen_kernels <output.inc>
+#include <algorithm>
 #include <cstdio>
 #include <map>
 #include <set>
@@ -68,6 +69,7 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   std::fprintf(f, "template <> struct TPCore<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
   std::fprintf(f, "  static constexpr int LMAX = %d, D1 = %d, D2 = %d, NP = %d, NNZ = %d;\n", t.lmax, t.d1, t.d2, np,
                int(t.entries.size()));
+  std::fprintf(f, "  static constexpr bool FULL = %s;\n", t.full_parity ? "true" : "false");
   // x irrep of each component (the per-irrep channel mixing acts block by block)
   std::fprintf(f, "  static constexpr int NX = %d;\n  static constexpr int XIRREP[%d] = {", int(t.x_irreps.size()), t.d1);
   for (int a = 0, k = 0; a < int(t.x_irreps.size()); ++a)
@@ -209,6 +211,81 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
   std::fprintf(f, "  }\n};\n\n");
 }
 
+// The forward as a per-center matrix: out[k] = sum_i M[k][i] x[i] with
+//   M[k][i] = sum_{p = (a(i), b, c(k))} W(p) sum_j C_pijk env[j],
+// which depends only on the center and the channel.  Its rows are split over
+// NW waves (ROWS consecutive rows each); wave w builds its rows once per
+// center and applies them to every edge.  Emitted for lmax 3, where it takes
+// about half the arithmetic of the direct contraction per edge.
+void emit_mfwd(FILE *f, const allegro::TPTable &t, int nw) {
+  const int d1 = t.d1, rows = d1 / nw;
+  // (k, i) -> list of (path, j, C)
+  std::map<std::pair<int, int>, std::vector<allegro::CGEntry>> cells;
+  for (const auto &e : t.entries) cells[{e.k, e.i}].push_back(e);
+  int maxm = 0;
+  std::vector<std::vector<std::pair<int, int>>> wave_cells(nw);
+  for (int w = 0; w < nw; ++w) {
+    for (const auto &kv : cells)
+      if (kv.first.first / rows == w) wave_cells[w].push_back(kv.first);
+    maxm = std::max(maxm, int(wave_cells[w].size()));
+  }
+  std::fprintf(f, "template <> struct TPMFwd<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
+  std::fprintf(f, "  static constexpr int NW = %d, ROWS = %d, MAXM = %d;\n", nw, rows, maxm);
+  // build
+  std::fprintf(f, "  template <class WT>\n  static __device__ __forceinline__ void build(int w, const float *__restrict__ env, "
+                  "const WT &W, float (&m)[MAXM]) {\n    switch (w) {\n");
+  for (int w = 0; w < nw; ++w) {
+    std::fprintf(f, "      case %d: {\n", w);
+    for (int q = 0; q < int(wave_cells[w].size()); ++q) {
+      const auto &es = cells[wave_cells[w][q]];
+      std::map<int, std::vector<allegro::CGEntry>> by_path;
+      for (const auto &e : es) by_path[e.path].push_back(e);
+      std::fprintf(f, "        {");
+      bool first_p = true;
+      for (const auto &pv : by_path) {
+        std::fprintf(f, " { float s;");
+        bool first = true;
+        for (const auto &e : pv.second) {
+          std::fprintf(f, " %s", accumulate("s", first, e.value, "env[" + std::to_string(e.j) + "]").c_str());
+          first = false;
+        }
+        if (first_p)
+          std::fprintf(f, " m[%d] = W(%d) * s; }", q, pv.first);
+        else
+          std::fprintf(f, " m[%d] = __builtin_fmaf(W(%d), s, m[%d]); }", q, pv.first, q);
+        first_p = false;
+      }
+      std::fprintf(f, " }\n");
+    }
+    for (int q = int(wave_cells[w].size()); q < maxm; ++q) std::fprintf(f, "        m[%d] = 0.0f;\n", q);
+    std::fprintf(f, "      } break;\n");
+  }
+  std::fprintf(f, "      default: break;\n    }\n  }\n");
+  // apply: one FMA chain per row of the wave, over the lane's x row in registers
+  std::fprintf(f, "  static __device__ __forceinline__ void apply(int w, const float (&x)[%d], const float (&m)[MAXM], "
+                  "float (&o)[ROWS]) {\n    switch (w) {\n", d1);
+  for (int w = 0; w < nw; ++w) {
+    std::fprintf(f, "      case %d:\n", w);
+    for (int r = 0; r < rows; ++r) {
+      const int k = w * rows + r;
+      std::fprintf(f, "        o[%d] =", r);
+      bool first = true;
+      std::string expr;
+      for (int q = 0; q < int(wave_cells[w].size()); ++q) {
+        if (wave_cells[w][q].first != k) continue;
+        const int i = wave_cells[w][q].second;
+        const std::string term = "m[" + std::to_string(q) + "], x[" + std::to_string(i) + "]";
+        expr = first ? "m[" + std::to_string(q) + "] * x[" + std::to_string(i) + "]"
+                     : "__builtin_fmaf(" + term + ", " + expr + ")";
+        first = false;
+      }
+      std::fprintf(f, " %s;\n", first ? "0.0f" : expr.c_str());
+    }
+    std::fprintf(f, "        break;\n");
+  }
+  std::fprintf(f, "      default: break;\n    }\n  }\n};\n\n");
+}
+
 }  // namespace
 
 int main(int argc, char **argv) {
@@ -224,10 +301,12 @@ int main(int argc, char **argv) {
   std::fprintf(f,
                "// Generated by gen_kernels from the sparse coupling table of cg_builder. Do not edit.\n"
                "#pragma once\n\n"
-               "template <int LMAX, bool FULL> struct TPCore;\n\n");
+               "template <int LMAX, bool FULL> struct TPCore;\n"
+               "template <int LMAX, bool FULL> struct TPMFwd;\n\n");
   try {
     for (int lmax = 1; lmax <= 3; ++lmax)
       for (int full = 0; full <= 1; ++full) emit_core(f, allegro::build_table(lmax, full != 0));
+    for (int full = 0; full <= 1; ++full) emit_mfwd(f, allegro::build_table(3, full != 0), 8);
   } catch (const std::exception &ex) {
     std::fprintf(stderr, "gen_kernels: %s\n", ex.what());
     std::fclose(f);
