@@ -304,15 +304,16 @@ struct KernelTraits {
 // regions are few and contiguous: a standalone probe of the forward's access
 // pattern measured 4.98 TB/s with one wave per center and 5.51 TB/s with 16.
 // That pays where the kernel is HBM-bound (lmax <= 2, and the lmax-3
-// backward at 128 channels).  Where it is bound by VALU issue (lmax 3 at 64
-// channels, and the forward at lmax 3), fewer waves per center leave room
-// for more workgroups per compute unit, which overlap one center's reduction
-// phases with another's streaming.  The counts are the fastest of 1, 2, 4, 8
-// and 16 measured for each kernel on the MI355X.
+// backward at 128 channels).  Where it is bound by VALU issue (the lmax-3
+// backward at 64 channels), fewer waves per center leave room for more
+// workgroups per compute unit, which overlap one center's reduction phases
+// with another's streaming.  The counts are the fastest of 1, 2, 4, 8 and 16
+// measured for each kernel on the MI355X.  (The lmax-3 forward is
+// tp_forward_m_kernel, whose 8 waves split the rows of a per-center matrix.)
 template <class Core, int U>
 struct TPWaves {
   static constexpr bool kHigh = Core::LMAX >= 3, kWide = U > 64;
-  static constexpr int kFwd = kHigh ? 2 : 16;
+  static constexpr int kFwd = 16;  // lmax <= 2
   static constexpr int bwd(bool wg) { return wg ? (kHigh && !kWide ? 2 : 4) : (kHigh ? (kWide ? 8 : 4) : 16); }
 };
 
