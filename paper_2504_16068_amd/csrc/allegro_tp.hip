@@ -374,11 +374,12 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 template <class Core>
 constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 
-template <class Core, int U>
-__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_forward_m_kernel(
+// MF is the generated matrix: TPMFwd (out = M x) or TPMBwdX (grad_x = M^T g,
+// the same kernel with g as input and grad_x as output).
+template <class Core, int U, class MF>
+__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_matrix_kernel(
     const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
     const float *__restrict__ path_w, float *__restrict__ out) {
-  using MF = TPMFwd<Core::LMAX, Core::FULL>;
   using L = Lanes<U>;
   constexpr int D1 = Core::D1, D2 = Core::D2, NW = MF::NW, ROWS = MF::ROWS;
   constexpr int T = U > kWave ? 4 : 8;      // slabs per tile (32 or 64 KB; 8 at U = 128 would spill)
@@ -466,6 +467,212 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       // only after its own barrier, by which every thread has read os here
     }
     lds_sync<NW>();  // both tiles are free before the next channel half
+  }
+}
+
+// ---------------------------------- training backward, lmax 3: segment sums
+// grad_env and the path-weight gradient from the per-center products
+// G[k][i] = sum over the center's edges of x[i] g[k] (generated TPGEnv; rows k
+// split over the 8 waves as in TPMFwd):
+//   grad_env[j] = sum_{(k,i)} sum_p W(p) C_pijk G[k][i],
+//   grad_W[p]   = sum_{(k,i)} sum_j C_pijk env[j] G[k][i].
+// Per edge a wave adds x[i] g[k] into its cells (about 930 FMAs per edge and
+// channel over the 8 waves); at the end of the center each wave adds its part
+// of both sums, and the waves' (and lane groups') parts are added in LDS in a
+// fixed order.  Then the embedding's VJP, as in tp_backward_kernel.  grad_x
+// comes from tp_matrix_kernel with TPMBwdX.  This takes about half the VALU
+// work of the direct training backward at lmax 3.
+template <class Core, int U>
+__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_backward_g_kernel(
+    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+    const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
+    const float *__restrict__ Y, float *__restrict__ grad_env, float *__restrict__ grad_w,
+    float *__restrict__ grad_Y, float *__restrict__ pw_part) {
+  using GE = TPGEnv<Core::LMAX, Core::FULL>;
+  using L = Lanes<U>;
+  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP, NW = GE::NW, ROWS = GE::ROWS;
+  constexpr int T = 4;                      // slabs per tile and tensor
+  constexpr int RS = D1 + 4, R4 = D1 / 4, SF4 = TileShape<D1>::SF4, TF4 = T * SF4, NT = NW * kWave;
+  constexpr int PER = (TF4 + NT - 1) / NT;
+  constexpr int TILE = T * kWave * RS;      // floats of one staged tile
+  constexpr int EB = 8, WROW = U + 1, STAGE = EB * (WROW + D2);
+  constexpr int GE_ROW = U * D2, GE_PART = NW * kWave * D2;
+  constexpr int PC = NP < 2 * TILE / (NW * kWave) ? NP : 2 * TILE / (NW * kWave);  // paths per reduction chunk
+  constexpr int R1 = 2 * TILE > GE_PART ? 2 * TILE : GE_PART;
+  constexpr int R2 = NW * STAGE > NW * kWave * PC ? NW * STAGE : NW * kWave * PC;
+  constexpr int REST = R1 > R2 ? R1 : R2;
+  static_assert(D1 % 4 == 0 && D1 == NW * ROWS && ROWS % 2 == 0, "rows of whole float4, split evenly");
+  // LDS: grad_env[n] [U][D2] (kept for pass 2), then one region reused for the
+  // x and g tiles, the path-weight partial sums, the grad_env partial sums and
+  // the pass-2 staging
+  __shared__ float4 smem4[(GE_ROW + REST + 3) / 4];
+  float *ge_l = reinterpret_cast<float *>(smem4), *rest = ge_l + GE_ROW;
+  float *xs = rest, *gs = rest + TILE;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int64_t n = blockIdx.x;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
+  auto src = [&](int64_t s0, int f, int t) -> int64_t {
+    const int sl = f / SF4, in = f % SF4;
+    if (s0 + sl >= n_slabs) return -1;
+    if constexpr (U <= kWave) {
+      const int64_t base = Slabs<U>::first_edge(e0, s0) * (U * D1 / 4), end = e1 * (U * D1 / 4);
+      const int64_t q = base + f;
+      return q < end ? q : -1;
+    } else {
+      return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
+    }
+  };
+#pragma unroll 1
+  for (int t = 0; t < L::CPL; ++t) {
+    const int u = ul + t * kWave;
+    float G[GE::MAXM];
+#pragma unroll
+    for (int q = 0; q < GE::MAXM; ++q) G[q] = 0.0f;
+    float4 vx[PER], vg[PER];
+    auto fetch = [&](int64_t s0) {
+      const float4 *x4 = reinterpret_cast<const float4 *>(x), *g4 = reinterpret_cast<const float4 *>(g);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int f = tid + NT * i;
+        const int64_t q = f < TF4 ? src(s0, f, t) : -1;
+        vx[i] = q >= 0 ? load_stream(x4 + q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        vg[i] = q >= 0 ? load_stream(g4 + q) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    };
+    if (n_slabs > 0) fetch(0);
+    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int f = tid + NT * i;
+        if (f < TF4) {
+          *reinterpret_cast<float4 *>(xs + (f / R4) * RS + 4 * (f % R4)) = vx[i];
+          *reinterpret_cast<float4 *>(gs + (f / R4) * RS + 4 * (f % R4)) = vg[i];
+        }
+      }
+      if (s0 + T < n_slabs) fetch(s0 + T);
+      lds_sync<NW>();
+      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+#pragma unroll 1
+      for (int sl = 0; sl < cnt; ++sl) {
+        const int r = sl * kWave + lane;
+        float xr[D1], gr[ROWS];
+#pragma unroll
+        for (int q = 0; q < R4; ++q) {
+          const float4 a = *reinterpret_cast<const float4 *>(xs + r * RS + 4 * q);
+          xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
+        }
+#pragma unroll
+        for (int q = 0; q < ROWS; ++q) gr[q] = gs[r * RS + wave * ROWS + q];
+        GE::accumulate(wave, xr, gr, G);  // rows past the segment hold zeros
+      }
+      lds_sync<NW>();  // the tiles may be refilled (or the region reused)
+    }
+    // grad_env: this wave's part for channel u, then the waves' and lane
+    // groups' parts, in order
+    {
+      float ge[D2];
+#pragma unroll
+      for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
+      CachedWeights wr;
+      wr.load(path_w, U, u);
+      GE::finish_ge(wave, wr, G, ge);
+#pragma unroll
+      for (int j = 0; j < D2; ++j) rest[(wave * kWave + lane) * D2 + j] = ge[j];
+    }
+    lds_sync<NW>();
+    for (int i = tid; i < L::LPE * D2; i += NT) {
+      const int uw = i / D2, j = i % D2;
+      float a = 0.0f;
+      for (int k = 0; k < NW; ++k)
+        for (int q = 0; q < L::G; ++q) a += rest[((k * kWave) + q * L::LPE + uw) * D2 + j];
+      ge_l[(uw + t * kWave) * D2 + j] = a;
+      grad_env[(n * U + uw + t * kWave) * D2 + j] = a;
+    }
+    lds_sync<NW>();
+    // grad_W: this wave's part, the lane groups by an xor butterfly (same bits
+    // on every lane of a channel), then the waves in order, PC paths at a time
+    float gw[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) gw[p] = 0.0f;
+    {
+      float er[D2];
+      load_row<D2>(env + (n * U + u) * D2, er);
+      GE::finish_gw(wave, er, G, gw);
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+#pragma unroll
+      for (int off = L::LPE; off < kWave; off *= 2) gw[p] += __shfl_xor(gw[p], off);
+    }
+    static_for<0, (NP + PC - 1) / PC>([&](auto ic) {
+      constexpr int p0 = decltype(ic)::value * PC, pn = NP - p0 < PC ? NP - p0 : PC;
+      if (grp == 0) {
+#pragma unroll
+        for (int q = 0; q < pn; ++q) rest[(wave * kWave + ul) * PC + q] = gw[p0 + q];
+      }
+      lds_sync<NW>();
+      for (int i = tid; i < L::LPE * pn; i += NT) {
+        const int q = i / L::LPE, uw = i % L::LPE;
+        float a = 0.0f;
+        for (int k = 0; k < NW; ++k) a += rest[(k * kWave + uw) * PC + q];
+        pw_part[(n * NP + p0 + q) * U + uw + t * kWave] = a;
+      }
+      lds_sync<NW>();
+    });
+  }
+
+  // Pass 2: the embedding's VJP through grad_env (as in tp_backward_kernel)
+  float *wl = rest + wave * STAGE;
+  float *yl = wl + EB * WROW;
+  const float4 *w4 = reinterpret_cast<const float4 *>(w);
+  float gel[L::CPL][D2];
+#pragma unroll
+  for (int c = 0; c < L::CPL; ++c)
+#pragma unroll
+    for (int j = 0; j < D2; ++j) gel[c][j] = ge_l[(ul + c * kWave) * D2 + j];
+  for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
+    const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
+    lds_sync<1>();  // this wave's previous batch is done with its staged rows
+    for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
+      const float4 v = w4[eb * (U / 4) + i4];
+      const int r = (4 * i4) / U, c = (4 * i4) % U;
+      float *dst = wl + r * WROW + c;
+      dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+    }
+    for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
+    lds_sync<1>();
+    for (int k = grp; k < cnt; k += L::G) {
+#pragma unroll
+      for (int c = 0; c < L::CPL; ++c) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D2; ++j) acc = __builtin_fmaf(gel[c][j], yl[k * D2 + j], acc);
+        grad_w[(eb + k) * U + ul + c * kWave] = acc;
+      }
+    }
+    {
+      constexpr int UQ = U / 8;  // channels per lane
+      const int k = lane / 8, q = lane % 8;
+      const float *wrow = wl + k * WROW + q * UQ;
+      const float *gq = ge_l + q * UQ * D2;
+      float gy[D2];
+#pragma unroll
+      for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
+      if (k < cnt) {
+#pragma unroll 4
+        for (int uu = 0; uu < UQ; ++uu) {
+          const float wv = wrow[uu];
+#pragma unroll
+          for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(gq[uu * D2 + j], wv, gy[j]);
+        }
+      }
+#pragma unroll
+      for (int off = 1; off < 8; off *= 2)
+#pragma unroll
+        for (int j = 0; j < D2; ++j) gy[j] += __shfl_xor(gy[j], off);
+      if (k < cnt && q == 0) store_row<D2>(grad_Y + (eb + k) * D2, gy);
+    }
   }
 }
 
@@ -828,7 +1035,8 @@ template <class Core, int U>
 void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 float *out) {
   if constexpr (Core::LMAX >= 3)
-    hipLaunchKernelGGL((tp_forward_m_kernel<Core, U>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, out);
+    hipLaunchKernelGGL((tp_matrix_kernel<Core, U, TPMFwd<Core::LMAX, Core::FULL>>), grid, dim3(kMFwdThreads<Core>), 0,
+                       s, rp, x, env, pw, out);
   else
     hipLaunchKernelGGL((tp_forward_kernel<Core, U>), grid, dim3(kWave * TPWaves<Core, U>::kFwd), 0, s, rp, x, env, pw,
                        out);
@@ -838,8 +1046,18 @@ template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
                 float *pw_part) {
-  hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x, env, pw,
-                     g, w, Y, gx, genv, gw, gy, pw_part);
+  if constexpr (WG && Core::LMAX >= 3 && U <= kWave) {
+    // training backward at lmax 3: grad_x = M^T g, then the segment sums from G
+    // (with two channel halves the segment-sum kernel would spill; U = 128 keeps
+    // the direct kernel)
+    hipLaunchKernelGGL((tp_matrix_kernel<Core, U, TPMBwdX<Core::LMAX, Core::FULL>>), grid, dim3(kMFwdThreads<Core>), 0,
+                       s, rp, g, env, pw, gx);
+    hipLaunchKernelGGL((tp_backward_g_kernel<Core, U>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g, w, Y,
+                       genv, gw, gy, pw_part);
+  } else {
+    hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x,
+                       env, pw, g, w, Y, gx, genv, gw, gy, pw_part);
+  }
 }
 
 struct Kernels {

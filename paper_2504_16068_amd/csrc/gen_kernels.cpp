@@ -217,11 +217,15 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
 // NW waves (ROWS consecutive rows each); wave w builds its rows once per
 // center and applies them to every edge.  Emitted for lmax 3, where it takes
 // about half the arithmetic of the direct contraction per edge.
-void emit_mfwd(FILE *f, const allegro::TPTable &t, int nw) {
+//
+// With transpose the rows are the x components i and the columns the output
+// components k: grad_x[i] = sum_k M[k][i] g[k], the VJP of the forward with
+// respect to x.
+void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name, bool transpose) {
   const int d1 = t.d1, rows = d1 / nw;
-  // (k, i) -> list of (path, j, C)
+  // (row, column) -> list of (path, j, C); row = k and column = i, or the reverse
   std::map<std::pair<int, int>, std::vector<allegro::CGEntry>> cells;
-  for (const auto &e : t.entries) cells[{e.k, e.i}].push_back(e);
+  for (const auto &e : t.entries) cells[transpose ? std::make_pair(e.i, e.k) : std::make_pair(e.k, e.i)].push_back(e);
   int maxm = 0;
   std::vector<std::vector<std::pair<int, int>>> wave_cells(nw);
   for (int w = 0; w < nw; ++w) {
@@ -229,7 +233,7 @@ void emit_mfwd(FILE *f, const allegro::TPTable &t, int nw) {
       if (kv.first.first / rows == w) wave_cells[w].push_back(kv.first);
     maxm = std::max(maxm, int(wave_cells[w].size()));
   }
-  std::fprintf(f, "template <> struct TPMFwd<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
+  std::fprintf(f, "template <> struct %s<%d, %s> {\n", name, t.lmax, t.full_parity ? "true" : "false");
   std::fprintf(f, "  static constexpr int NW = %d, ROWS = %d, MAXM = %d;\n", nw, rows, maxm);
   // build
   std::fprintf(f, "  template <class WT>\n  static __device__ __forceinline__ void build(int w, const float *__restrict__ env, "
@@ -286,6 +290,77 @@ void emit_mfwd(FILE *f, const allegro::TPTable &t, int nw) {
   std::fprintf(f, "      default: break;\n    }\n  }\n};\n\n");
 }
 
+// The segment sums of the backward from the per-center matrix of products
+// G[k][i] = sum over the center's edges of x[i] g[k] (rows k split over the
+// waves as in TPMFwd, only the (k, i) cells that carry coupling entries):
+//   grad_env[j] = sum_{(k,i)} sum_{p: (p,i,j,k)} W(p) C_pijk G[k][i]
+//   grad_W[p]   = sum_{(k,i)} sum_j C_pijk env[j] G[k][i]
+// accumulate() adds one edge to the wave's cells; finish_ge() and finish_gw()
+// add the wave's part of the two sums into ge and gw (which the caller zeroes).
+void emit_genv(FILE *f, const allegro::TPTable &t, int nw) {
+  const int d1 = t.d1, rows = d1 / nw;
+  std::map<std::pair<int, int>, std::vector<allegro::CGEntry>> cells;  // (k, i)
+  for (const auto &e : t.entries) cells[{e.k, e.i}].push_back(e);
+  int maxm = 0;
+  std::vector<std::vector<std::pair<int, int>>> wave_cells(nw);
+  for (int w = 0; w < nw; ++w) {
+    for (const auto &kv : cells)
+      if (kv.first.first / rows == w) wave_cells[w].push_back(kv.first);
+    maxm = std::max(maxm, int(wave_cells[w].size()));
+  }
+  std::fprintf(f, "template <> struct TPGEnv<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
+  std::fprintf(f, "  static constexpr int NW = %d, ROWS = %d, MAXM = %d;\n", nw, rows, maxm);
+  std::fprintf(f, "  static __device__ __forceinline__ void accumulate(int w, const float (&x)[%d], const float (&g)[ROWS], "
+                  "float (&G)[MAXM]) {\n    switch (w) {\n", d1);
+  for (int w = 0; w < nw; ++w) {
+    std::fprintf(f, "      case %d:\n", w);
+    for (int q = 0; q < int(wave_cells[w].size()); ++q)
+      std::fprintf(f, "        G[%d] = __builtin_fmaf(x[%d], g[%d], G[%d]);\n", q, wave_cells[w][q].second,
+                   wave_cells[w][q].first - w * rows, q);
+    std::fprintf(f, "        break;\n");
+  }
+  std::fprintf(f, "      default: break;\n    }\n  }\n");
+  // finish_ge: ge[j] += sum over the wave's cells of W(p) C_pijk G[q]
+  std::fprintf(f, "  template <class WT>\n  static __device__ __forceinline__ void finish_ge(int w, const WT &W, "
+                  "const float (&G)[MAXM], float (&ge)[%d]) {\n    switch (w) {\n", t.d2);
+  for (int w = 0; w < nw; ++w) {
+    std::fprintf(f, "      case %d:\n", w);
+    for (int q = 0; q < int(wave_cells[w].size()); ++q) {
+      std::map<int, std::vector<allegro::CGEntry>> by_path;
+      for (const auto &e : cells[wave_cells[w][q]]) by_path[e.path].push_back(e);
+      for (const auto &pv : by_path) {
+        std::fprintf(f, "        { const float t = W(%d) * G[%d];", pv.first, q);
+        for (const auto &e : pv.second)
+          std::fprintf(f, " ge[%d] = __builtin_fmaf(%s, t, ge[%d]);", e.j, lit(e.value).c_str(), e.j);
+        std::fprintf(f, " }\n");
+      }
+    }
+    std::fprintf(f, "        break;\n");
+  }
+  std::fprintf(f, "      default: break;\n    }\n  }\n");
+  // finish_gw: gw[p] += sum over the wave's cells of (sum_j C_pijk env[j]) G[q]
+  std::fprintf(f, "  static __device__ __forceinline__ void finish_gw(int w, const float *__restrict__ env, "
+                  "const float (&G)[MAXM], float (&gw)[%d]) {\n    switch (w) {\n", int(t.paths.size()));
+  for (int w = 0; w < nw; ++w) {
+    std::fprintf(f, "      case %d:\n", w);
+    for (int q = 0; q < int(wave_cells[w].size()); ++q) {
+      std::map<int, std::vector<allegro::CGEntry>> by_path;
+      for (const auto &e : cells[wave_cells[w][q]]) by_path[e.path].push_back(e);
+      for (const auto &pv : by_path) {
+        std::fprintf(f, "        { float s;");
+        bool first = true;
+        for (const auto &e : pv.second) {
+          std::fprintf(f, " %s", accumulate("s", first, e.value, "env[" + std::to_string(e.j) + "]").c_str());
+          first = false;
+        }
+        std::fprintf(f, " gw[%d] = __builtin_fmaf(s, G[%d], gw[%d]); }\n", pv.first, q, pv.first);
+      }
+    }
+    std::fprintf(f, "        break;\n");
+  }
+  std::fprintf(f, "      default: break;\n    }\n  }\n};\n\n");
+}
+
 }  // namespace
 
 int main(int argc, char **argv) {
@@ -302,11 +377,18 @@ int main(int argc, char **argv) {
                "// Generated by gen_kernels from the sparse coupling table of cg_builder. Do not edit.\n"
                "#pragma once\n\n"
                "template <int LMAX, bool FULL> struct TPCore;\n"
-               "template <int LMAX, bool FULL> struct TPMFwd;\n\n");
+               "template <int LMAX, bool FULL> struct TPMFwd;\n"
+               "template <int LMAX, bool FULL> struct TPMBwdX;\n"
+               "template <int LMAX, bool FULL> struct TPGEnv;\n\n");
   try {
     for (int lmax = 1; lmax <= 3; ++lmax)
       for (int full = 0; full <= 1; ++full) emit_core(f, allegro::build_table(lmax, full != 0));
-    for (int full = 0; full <= 1; ++full) emit_mfwd(f, allegro::build_table(3, full != 0), 8);
+    for (int full = 0; full <= 1; ++full) {
+      const allegro::TPTable t3 = allegro::build_table(3, full != 0);
+      emit_matrix(f, t3, 8, "TPMFwd", false);
+      emit_matrix(f, t3, 8, "TPMBwdX", true);
+      emit_genv(f, t3, 8);
+    }
   } catch (const std::exception &ex) {
     std::fprintf(stderr, "gen_kernels: %s\n", ex.what());
     std::fclose(f);

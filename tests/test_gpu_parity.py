@@ -225,7 +225,7 @@ def test_skewed_degrees(at, lmax, full, U):
     _note(f"skewed lmax{lmax} U{U}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
     assert errs["out"] <= FWD_TOL
     assert all(v <= BWD_TOL for k, v in errs.items() if k != "out"), errs
-    assert _same_bits(gx, grads[0])
+    assert block_rel_err(gx.cpu().numpy(), ref_g[0], t.x_slices) <= BWD_TOL
 
 
 def test_no_edges_gives_zero_env_and_grad_env(at):
@@ -388,16 +388,17 @@ def test_train_backward_parity(at, case):
     env = at.allegro_env_embed(plan, rp, wd, yd)
     base = at.allegro_tp_backward(plan, rp, xd, env, pwd, gd, wd, yd)
     (gx, genv, gw, gy, gpw), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
-    # grad_x is per edge: bit for bit that of the inference backward; the segment
-    # sums (grad_env and through it grad_w, grad_Y) split the edges over a
-    # different number of waves, so they agree to fp32 rounding, and both match
-    # the oracle
-    assert _same_bits(gx, base[0])
+    # the training backward splits the work differently from the inference
+    # backward (other wave counts; at lmax 3 a per-center matrix for grad_x and
+    # per-center products for the segment sums), so its gradients agree with the
+    # inference ones to fp32 rounding; both match the oracle
     t = otp.TensorProduct(lmax, full)
     renv = otp.env_embed(data[0], data[2], data[3])
     ref = t.backward(data[0], data[1], renv, data[4], data[5], data[2], data[3])
-    for got, r, blocks in zip((genv, gw, gy), ref[1:], (t.env_slices, None, t.env_slices)):
+    for got, r, blocks in zip((gx, genv, gw, gy), ref, (t.x_slices, t.env_slices, None, t.env_slices)):
         assert block_rel_err(got.cpu().numpy(), r, blocks) <= BWD_TOL
+    for got, b in zip((gx, genv, gw, gy), base):
+        assert block_rel_err(got.cpu().numpy(), b.cpu().numpy()) <= BWD_TOL
     ref = t.path_weight_grad(data[0], data[1], otp.env_embed(data[0], data[2], data[3]), data[5])
     err = block_rel_err(gpw.cpu().numpy(), ref)
     _note(f"training backward {case}: grad_path_w err={err:.2e}")
@@ -447,10 +448,7 @@ def test_train_backward_full_size(at, name, n_samples=16):
     pw = workloads.path_weights(cfg)
     rp, yd, pwd = _t(graph.row_ptr), _t(graph.Y), _t(pw)
     env = at.allegro_env_embed(plan, rp, w, yd)
-    base_gx = at.allegro_tp_backward(plan, rp, x, env, pwd, g, w, yd)[0]
     (gx, _, _, _, gpw), ws = _train(at, plan, rp, x, env, pwd, g, w, yd)
-    assert _same_bits(gx, base_gx)
-    del gx, base_gx
     n, cols = graph.n_atoms, plan.n_paths * cfg.U
     part = ws[: n * cols * 4].view(torch.float32).view(n, plan.n_paths, cfg.U)
     rng = np.random.default_rng(cfg.index + 50)
@@ -460,8 +458,12 @@ def test_train_backward_full_size(at, name, n_samples=16):
         s, e = int(graph.row_ptr[c]), int(graph.row_ptr[c + 1])
         xs, ws_, gs = x[s:e].cpu().numpy(), w[s:e].cpu().numpy(), g[s:e].cpu().numpy()
         local = np.array([0, e - s], np.int64)
-        ref = t.path_weight_grad(local, xs, otp.env_embed(local, ws_, graph.Y[s:e]), gs)
+        env_c = otp.env_embed(local, ws_, graph.Y[s:e])
+        ref = t.path_weight_grad(local, xs, env_c, gs)
         assert block_rel_err(part[c].cpu().numpy(), ref) <= BWD_TOL, c
+        ref_gx = t.backward(local, xs, env_c, pw, gs, ws_, graph.Y[s:e])[0]
+        assert block_rel_err(gx[s:e].cpu().numpy(), ref_gx, t.x_slices) <= BWD_TOL, c
+    del gx
     ph = part.cpu().numpy().astype(np.float64).reshape(n, cols)
     total = ph.sum(axis=0)
     # recursive-summation bound: at most ceil(ceil(N / 128) / 4) + 130 sequential fp32 additions
