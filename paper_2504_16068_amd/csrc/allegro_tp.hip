@@ -482,7 +482,10 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
 // fixed order.  Then the embedding's VJP, as in tp_backward_kernel.  grad_x
 // comes from tp_matrix_kernel with TPMBwdX.  This takes about half the VALU
 // work of the direct training backward at lmax 3.
-template <class Core, int U>
+// With U = 128 the two channel halves are two launches (HALF = 0, then 1; one
+// launch handling both would spill): the first writes half 0's grad_env, the
+// second reads it back for the embedding's VJP, which it alone performs.
+template <class Core, int U, int HALF>
 __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_backward_g_kernel(
     const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
     const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
@@ -523,8 +526,9 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
     }
   };
-#pragma unroll 1
-  for (int t = 0; t < L::CPL; ++t) {
+  static_assert(L::CPL == 1 || L::CPL == 2, "one or two channel halves");
+  {
+    constexpr int t = HALF;
     const int u = ul + t * kWave;
     float G[GE::MAXM];
 #pragma unroll
@@ -622,6 +626,12 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
     });
   }
 
+  if constexpr (L::CPL == 2) {
+    if constexpr (HALF == 0) return;  // the second launch does pass 2
+    // half 0 of grad_env[n], written by the first launch
+    for (int i = tid; i < kWave * D2; i += NT) ge_l[i] = grad_env[n * U * D2 + i];
+    lds_sync<NW>();
+  }
   // Pass 2: the embedding's VJP through grad_env (as in tp_backward_kernel)
   float *wl = rest + wave * STAGE;
   float *yl = wl + EB * WROW;
@@ -1046,14 +1056,15 @@ template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
                 float *pw_part) {
-  if constexpr (WG && Core::LMAX >= 3 && U <= kWave) {
+  if constexpr (WG && Core::LMAX >= 3) {
     // training backward at lmax 3: grad_x = M^T g, then the segment sums from G
-    // (with two channel halves the segment-sum kernel would spill; U = 128 keeps
-    // the direct kernel)
     hipLaunchKernelGGL((tp_matrix_kernel<Core, U, TPMBwdX<Core::LMAX, Core::FULL>>), grid, dim3(kMFwdThreads<Core>), 0,
                        s, rp, g, env, pw, gx);
-    hipLaunchKernelGGL((tp_backward_g_kernel<Core, U>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g, w, Y,
-                       genv, gw, gy, pw_part);
+    hipLaunchKernelGGL((tp_backward_g_kernel<Core, U, 0>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g, w,
+                       Y, genv, gw, gy, pw_part);
+    if constexpr (U > kWave)
+      hipLaunchKernelGGL((tp_backward_g_kernel<Core, U, 1>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g,
+                         w, Y, genv, gw, gy, pw_part);
   } else {
     hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x,
                        env, pw, g, w, Y, gx, genv, gw, gy, pw_part);
