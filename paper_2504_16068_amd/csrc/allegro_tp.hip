@@ -271,9 +271,8 @@ struct RegWeights {
   __device__ __forceinline__ float operator()(int p) const { return r[p]; }
 };
 
-// Path weights read at use from the lane's column of path_w (an L1/L2 hit after
-// the first edge) instead of NP registers; renew() hides the pointer from
-// loop-invariant code motion so the loads are not hoisted back into registers.
+// Path weights read at use from the lane's column of path_w (an L1/L2 hit)
+// instead of NP registers, for code run once per center.
 struct CachedWeights {
   typedef const __attribute__((address_space(1))) float *gptr;
   gptr col;
@@ -282,7 +281,6 @@ struct CachedWeights {
     col = (gptr)(path_w + u);
     U = U_;
   }
-  __device__ __forceinline__ void renew() { asm volatile("" : "+v"(col)); }
   __device__ __forceinline__ float operator()(int p) const { return col[p * U]; }
 };
 
@@ -291,9 +289,6 @@ struct KernelTraits {
   // waves per SIMD the register allocation must allow
   static constexpr int kFwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
   static constexpr int kBwdOccupancy = Core::LMAX >= 3 ? 2 : 4;
-  // the path-weight accumulators add NP live registers per lane; at lmax 3 the
-  // training variant makes room for them by reading the weights from cache
-  static constexpr bool cached_weights(bool wg) { return wg && Core::LMAX >= 3; }
   static constexpr int bwd_occupancy(bool wg) { return wg ? 2 : kBwdOccupancy; }
 };
 
@@ -308,13 +303,14 @@ struct KernelTraits {
 // backward at 64 channels), fewer waves per center leave room for more
 // workgroups per compute unit, which overlap one center's reduction phases
 // with another's streaming.  The counts are the fastest of 1, 2, 4, 8 and 16
-// measured for each kernel on the MI355X.  (The lmax-3 forward is
-// tp_forward_m_kernel, whose 8 waves split the rows of a per-center matrix.)
+// measured for each kernel on the MI355X.  (At lmax 3 the forward and the
+// training backward are tp_matrix_kernel and tp_backward_g_kernel, whose 8
+// waves split the rows of per-center matrices.)
 template <class Core, int U>
 struct TPWaves {
   static constexpr bool kHigh = Core::LMAX >= 3, kWide = U > 64;
   static constexpr int kFwd = 16;  // lmax <= 2
-  static constexpr int bwd(bool wg) { return wg ? (kHigh && !kWide ? 2 : 4) : (kHigh ? (kWide ? 8 : 4) : 16); }
+  static constexpr int bwd(bool wg) { return wg ? 4 : (kHigh ? (kWide ? 8 : 4) : 16); }
 };
 
 // ------------------------------------------------------ tensor product fwd
@@ -698,8 +694,7 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
                                           int t, int lane, float (&ge)[Core::D2], float (&sw)[Core::NP]) {
   constexpr int D1 = Core::D1, D2 = Core::D2, TF4 = TileShape<D1>::SF4;
   const int u = lane % Lanes<U>::LPE + t * kWave;
-  constexpr bool kCached = KernelTraits<Core>::cached_weights(WG);
-  typename std::conditional<kCached, CachedWeights, RegWeights<Core::NP>>::type wr;
+  RegWeights<Core::NP> wr;
   wr.load(path_w, U, u);
   float er[D2];
   load_row<D2>(env + (n * U + u) * D2, er);
@@ -715,7 +710,6 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
       // x row in, grad_x row out, in place in the LDS tile
       float *row = tx + lane * D1;
       const float *grow = tg + lane * D1;
-      if constexpr (kCached) wr.renew();
       if constexpr (WG) Core::wgrad(row, er, grow, sw);
       Core::bwd(row, er, wr, grow, row, ge);
     }
@@ -760,6 +754,7 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   using B = BwdLds<Core, U, WG, NW>;
   constexpr int D2 = Core::D2, NP = Core::NP, WPT = NW / L::CPL, NT = NW * kWave;
   static_assert(NW % L::CPL == 0, "waves split evenly over the channel halves");
+  static_assert(!WG || Core::LMAX <= 2, "the lmax-3 training backward is tp_backward_g_kernel");
   __shared__ float4 smem[(B::FLOATS + 3) / 4];
   float *lds = reinterpret_cast<float *>(smem);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
