@@ -478,6 +478,12 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
 // fixed order.  Then the embedding's VJP, as in tp_backward_kernel.  grad_x
 // comes from tp_matrix_kernel with TPMBwdX.  This takes about half the VALU
 // work of the direct training backward at lmax 3.
+// The register file holds one such workgroup per compute unit, so nothing else
+// streams while it is in the center-end phases.  To shorten them, the center's
+// env rows (and, in the second launch, half 0 of grad_env[n]) are staged in
+// LDS behind the first tile's loads, and the first embedding-VJP batch is
+// loaded before the sums are formed.  (Staging the path weights per center as
+// well was slower than reading them from cache at use.)
 // With U = 128 the two channel halves are two launches (HALF = 0, then 1; one
 // launch handling both would spill): the first writes half 0's grad_env, the
 // second reads it back for the embedding's VJP, which it alone performs.
@@ -500,12 +506,18 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
   constexpr int R1 = 2 * TILE > GE_PART ? 2 * TILE : GE_PART;
   constexpr int R2 = NW * STAGE > NW * kWave * PC ? NW * STAGE : NW * kWave * PC;
   constexpr int REST = R1 > R2 ? R1 : R2;
+  constexpr int LPE = L::LPE, ES = D2 + 1;  // env rows padded to D2 + 1 floats (distinct banks)
+  constexpr int ENV = LPE * ES;
+  constexpr int EF4 = LPE * D2 / 4, GF4 = HALF == 1 ? kWave * D2 / 4 : 0;
+  constexpr int SPER = (EF4 + GF4 + NT - 1) / NT;  // float4 per thread staged at the center's start
+  constexpr bool PASS2 = L::CPL == 1 || HALF == 1;
   static_assert(D1 % 4 == 0 && D1 == NW * ROWS && ROWS % 2 == 0, "rows of whole float4, split evenly");
-  // LDS: grad_env[n] [U][D2] (kept for pass 2), then one region reused for the
-  // x and g tiles, the path-weight partial sums, the grad_env partial sums and
-  // the pass-2 staging
-  __shared__ float4 smem4[(GE_ROW + REST + 3) / 4];
-  float *ge_l = reinterpret_cast<float *>(smem4), *rest = ge_l + GE_ROW;
+  static_assert(D2 % 4 == 0, "env rows of whole float4");
+  // LDS: this half's env[n] rows [LPE][D2 + 1]; grad_env[n] [U][D2] (kept for
+  // pass 2); then one region reused for the x and g tiles, the path-weight
+  // partial sums, the grad_env partial sums and the pass-2 staging
+  __shared__ float4 smem4[(ENV + GE_ROW + REST + 3) / 4];
+  float *envl = reinterpret_cast<float *>(smem4), *ge_l = envl + ENV, *rest = ge_l + GE_ROW;
   float *xs = rest, *gs = rest + TILE;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
   const int64_t n = blockIdx.x;
@@ -523,9 +535,26 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
     }
   };
   static_assert(L::CPL == 1 || L::CPL == 2, "one or two channel halves");
+  // one embedding-VJP batch (EB edges) of this wave in registers: w rows, Y rows
+  constexpr int P2W = (EB * U / 4 + kWave - 1) / kWave, P2Y = (EB * D2 + kWave - 1) / kWave;
+  float4 pv[PASS2 ? P2W : 1];
+  float py[PASS2 ? P2Y : 1];
+  auto p2_fetch = [&](int64_t eb) {
+    const int cnt = int(e1 - eb < EB ? (e1 - eb > 0 ? e1 - eb : 0) : EB);
+    const float4 *w4 = reinterpret_cast<const float4 *>(w);
+#pragma unroll
+    for (int q = 0; q < P2W; ++q) {
+      const int i4 = lane + kWave * q;
+      if (i4 < cnt * (U / 4)) pv[q] = w4[eb * (U / 4) + i4];
+    }
+#pragma unroll
+    for (int q = 0; q < P2Y; ++q) {
+      const int i = lane + kWave * q;
+      if (i < cnt * D2) py[q] = Y[eb * D2 + i];
+    }
+  };
   {
     constexpr int t = HALF;
-    const int u = ul + t * kWave;
     float G[GE::MAXM];
 #pragma unroll
     for (int q = 0; q < GE::MAXM; ++q) G[q] = 0.0f;
@@ -541,6 +570,30 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       }
     };
     if (n_slabs > 0) fetch(0);
+    {
+      // behind the first tile: this half's env[n] rows and (second launch) half
+      // 0 of grad_env[n]
+      float4 v[SPER];
+      const float4 *env4 = reinterpret_cast<const float4 *>(env + (n * U + t * kWave) * D2);
+      const float4 *ge4 = reinterpret_cast<const float4 *>(grad_env + n * U * D2);
+#pragma unroll
+      for (int i = 0; i < SPER; ++i) {
+        const int f = tid + NT * i;
+        if (f < EF4) v[i] = env4[f];
+        else if (f < EF4 + GF4) v[i] = ge4[f - EF4];
+      }
+#pragma unroll
+      for (int i = 0; i < SPER; ++i) {
+        const int f = tid + NT * i;
+        if (f < EF4) {
+          const int q = 4 * f, c = q / D2, j = q % D2;
+          float *d = envl + c * ES + j;
+          d[0] = v[i].x; d[1] = v[i].y; d[2] = v[i].z; d[3] = v[i].w;
+        } else if (f < EF4 + GF4) {
+          *reinterpret_cast<float4 *>(ge_l + 4 * (f - EF4)) = v[i];
+        }
+      }
+    }
     for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
@@ -568,6 +621,9 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       }
       lds_sync<NW>();  // the tiles may be refilled (or the region reused)
     }
+    if (n_slabs == 0) lds_sync<NW>();  // the staged rows are visible
+    // the first embedding-VJP batch of this wave, in flight while the sums form
+    if constexpr (PASS2) p2_fetch(e0 + int64_t(wave) * EB);
     // grad_env: this wave's part for channel u, then the waves' and lane
     // groups' parts, in order
     {
@@ -575,7 +631,7 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
 #pragma unroll
       for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
       CachedWeights wr;
-      wr.load(path_w, U, u);
+      wr.load(path_w, U, ul + t * kWave);
       GE::finish_ge(wave, wr, G, ge);
 #pragma unroll
       for (int j = 0; j < D2; ++j) rest[(wave * kWave + lane) * D2 + j] = ge[j];
@@ -597,7 +653,8 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
     for (int p = 0; p < NP; ++p) gw[p] = 0.0f;
     {
       float er[D2];
-      load_row<D2>(env + (n * U + u) * D2, er);
+#pragma unroll
+      for (int j = 0; j < D2; ++j) er[j] = envl[ul * ES + j];
       GE::finish_gw(wave, er, G, gw);
     }
 #pragma unroll
@@ -622,16 +679,11 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
     });
   }
 
-  if constexpr (L::CPL == 2) {
-    if constexpr (HALF == 0) return;  // the second launch does pass 2
-    // half 0 of grad_env[n], written by the first launch
-    for (int i = tid; i < kWave * D2; i += NT) ge_l[i] = grad_env[n * U * D2 + i];
-    lds_sync<NW>();
-  }
-  // Pass 2: the embedding's VJP through grad_env (as in tp_backward_kernel)
+  if constexpr (!PASS2) return;  // the second launch does pass 2
+  // Pass 2: the embedding's VJP through grad_env (as in tp_backward_kernel).
+  // (With two halves, half 0 of grad_env[n] was staged at the center's start.)
   float *wl = rest + wave * STAGE;
   float *yl = wl + EB * WROW;
-  const float4 *w4 = reinterpret_cast<const float4 *>(w);
   float gel[L::CPL][D2];
 #pragma unroll
   for (int c = 0; c < L::CPL; ++c)
@@ -640,13 +692,21 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
   for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
     lds_sync<1>();  // this wave's previous batch is done with its staged rows
-    for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
-      const float4 v = w4[eb * (U / 4) + i4];
-      const int r = (4 * i4) / U, c = (4 * i4) % U;
-      float *dst = wl + r * WROW + c;
-      dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+#pragma unroll
+    for (int q = 0; q < P2W; ++q) {
+      const int i4 = lane + kWave * q;
+      if (i4 < cnt * (U / 4)) {
+        const int r = (4 * i4) / U, c = (4 * i4) % U;
+        float *dst = wl + r * WROW + c;
+        dst[0] = pv[q].x; dst[1] = pv[q].y; dst[2] = pv[q].z; dst[3] = pv[q].w;
+      }
     }
-    for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
+#pragma unroll
+    for (int q = 0; q < P2Y; ++q) {
+      const int i = lane + kWave * q;
+      if (i < cnt * D2) yl[i] = py[q];
+    }
+    if (eb + int64_t(NW) * EB < e1) p2_fetch(eb + int64_t(NW) * EB);  // the next batch
     lds_sync<1>();
     for (int k = grp; k < cnt; k += L::G) {
 #pragma unroll
