@@ -383,6 +383,12 @@ __device__ __forceinline__ void mix_memory_role(int64_t E, int64_t n_tiles, cons
   using M = MixTile<X>;
   constexpr int U = M::U, D1 = M::D1, NE = M::NE, PER = M::PER, F4 = M::F4;
   const int mt = int(threadIdx.x) - 256;
+  // The thread's float4 of a tile: fi(i) = f0 + 16 i.  Each group of 16 lanes
+  // covers 256 contiguous bytes per access (coalesced), and a thread's float4
+  // lie 256 B apart, within the reach of one base address and immediate
+  // offsets (4 KB apart, as with fi(i) = mt + 256 i, measured 4% slower).
+  const int f0 = (mt / 16) * (16 * PER) + mt % 16;
+  auto fi = [&](int i) { return f0 + 16 * i; };
   // LDS offset (within a buffer) of each of the thread's elements: component k
   // of channel u of edge e sits in column NE off(c) + e dim(c) + m, row u
   int addr[PER][4];
@@ -390,7 +396,7 @@ __device__ __forceinline__ void mix_memory_role(int64_t E, int64_t n_tiles, cons
   for (int i = 0; i < PER; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = 4 * (mt + 256 * i) + q;
+      const int idx = 4 * fi(i) + q;
       int a = 0;
       if (idx < 4 * F4) {
         const int e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
@@ -406,14 +412,14 @@ __device__ __forceinline__ void mix_memory_role(int64_t E, int64_t n_tiles, cons
     const float4 *s4 = reinterpret_cast<const float4 *>(src + t * NE * U * D1);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int f = mt + 256 * i;
+      const int f = fi(i);
       v[i] = f < nf4 ? load_stream(s4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
   auto put = [&](float *b, const float4 (&v)[PER]) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      if (mt + 256 * i >= F4) continue;
+      if (fi(i) >= F4) continue;
       b[addr[i][0]] = v[i].x;
       b[addr[i][1]] = v[i].y;
       b[addr[i][2]] = v[i].z;
@@ -425,7 +431,7 @@ __device__ __forceinline__ void mix_memory_role(int64_t E, int64_t n_tiles, cons
     float4 *d4 = reinterpret_cast<float4 *>(dst + t * NE * U * D1);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int f = mt + 256 * i;
+      const int f = fi(i);
       if (f < nf4) store_stream(make_float4(b[addr[i][0]], b[addr[i][1]], b[addr[i][2]], b[addr[i][3]]), d4 + f);
     }
   };
@@ -532,13 +538,16 @@ __device__ __forceinline__ void wgrad_memory_role(int64_t E, int64_t n_tiles, co
   using M = WgTile<X>;
   constexpr int U = M::U, D1 = M::D1, NE = M::NE, PER = M::PER, F4 = M::F4;
   const int mt = int(threadIdx.x) - 256;
+  // the thread's float4 of a tile, 256 B apart (as in mix_memory_role)
+  const int f0 = (mt / 16) * (16 * PER) + mt % 16;
+  auto fi = [&](int i) { return f0 + 16 * i; };
   // LDS offset (within a tensor's tile) of each of the thread's elements
   int addr[PER][4];
 #pragma unroll
   for (int i = 0; i < PER; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = 4 * (mt + 256 * i) + q;
+      const int idx = 4 * fi(i) + q;
       int a = 0;
       if (idx < 4 * F4) {
         const int e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
@@ -555,7 +564,7 @@ __device__ __forceinline__ void wgrad_memory_role(int64_t E, int64_t n_tiles, co
     const float4 *b4 = reinterpret_cast<const float4 *>(tt + t * NE * U * D1);
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int f = mt + 256 * i;
+      const int f = fi(i);
       va[i] = f < nf4 ? load_stream(a4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
       vb[i] = f < nf4 ? load_stream(b4 + f) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
@@ -564,7 +573,7 @@ __device__ __forceinline__ void wgrad_memory_role(int64_t E, int64_t n_tiles, co
     float *la = b, *lb = b + M::COLS * M::CS;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      if (mt + 256 * i >= F4) continue;
+      if (fi(i) >= F4) continue;
       la[addr[i][0]] = va[i].x; la[addr[i][1]] = va[i].y; la[addr[i][2]] = va[i].z; la[addr[i][3]] = va[i].w;
       lb[addr[i][0]] = vb[i].x; lb[addr[i][1]] = vb[i].y; lb[addr[i][2]] = vb[i].z; lb[addr[i][3]] = vb[i].w;
     }
