@@ -266,8 +266,8 @@ def time_layer(torch, at, dev, reps, name="medium_layer"):
 def cpu_baseline(graph, host_inputs, edges_per_thread=24576, max_threads=16):
     """Time the fp64 oracle on a prefix of whole center segments of the workload.
 
-    One Python thread per host core (at most max_threads, the host's share on the
-    GPU machine), each running env_embed + forward + backward on its own range of
+    One Python thread per host core (at most max_threads, the host share of one
+    GPU), each running env_embed + forward + backward on its own range of
     whole segments with single-threaded BLAS; NumPy releases the GIL inside its
     array loops, so the threads run in parallel.  The single-thread rate on the
     first range is reported beside it.
@@ -334,7 +334,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the tensor product shards by center ranges with no "
-              "communication inside the path, and multi-GPU runs are not part of this build.", file=sys.stderr)
+              "communication inside the path; each GPU would run this on its own share.", file=sys.stderr)
         sys.exit(2)
 
     import torch
