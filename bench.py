@@ -104,9 +104,10 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
     copy_kib = (4 << 30) / 1024
 
     def per_launch(rows, kernel):
-        # the inference backward only (template flag false, then the waves per
-        # center), not the training variant
-        pat = re.compile(kernel + r"<.*,\s*false(,\s*\d+)?>")
+        # the inference backward only (template arguments: core (lmax, parity),
+        # U, the training flag false, then the waves per center), not the
+        # training variant
+        pat = re.compile(kernel + r"<TPCore<\d+,\s*(true|false)>,\s*\d+,\s*false(,\s*\d+)?>")
         vals = [float(r["Counter_Value"]) for r in rows if pat.search(r["Kernel_Name"])]
         return sum(vals) / len(vals), len(vals)
 
