@@ -174,6 +174,34 @@ def test_edge_cases(at, lmax, full, U, degrees):
     assert np.all(env[np.asarray(degrees) == 0] == 0)
 
 
+ALL_SHAPES = [(lmax, full, U) for lmax in (1, 2, 3) for full in (False, True) for U in (16, 32, 64, 128)]
+
+
+@pytest.mark.parametrize("lmax,full,U", ALL_SHAPES)
+def test_every_core_and_width(at, lmax, full, U):
+    """Every compiled (lmax, parity) core at every channel count, through the
+    embedding, the forward, the inference backward and the training backward,
+    on ragged segments (empty, one edge, a partial lane-group pass, more than
+    one slab), against the oracle."""
+    degrees = [0, 1, 3, 17, 66]
+    _note(f"[gpu] shape sweep lmax={lmax} full={full} U={U}")
+    data = _synthetic(lmax, full, U, degrees, seed=1000 + lmax * 100 + U + int(full))
+    plan = _plan(at, lmax, U, full)
+    gpu = _np(_run_gpu(at, plan, *data))
+    t, *ref = _oracle(lmax, full, *data)
+    _compare(t, gpu, ref, f"sweep lmax{lmax}{'F' if full else 'N'}U{U}")
+    rp, xd, wd, yd, pwd, gd = (_t(a) for a in data)
+    env = at.allegro_env_embed(plan, rp, wd, yd)
+    (gx, genv, gw, gy, gpw), _ = _train(at, plan, rp, xd, env, pwd, gd, wd, yd)
+    renv = otp.env_embed(data[0], data[2], data[3])
+    rgrads = t.backward(data[0], data[1], renv, data[4], data[5], data[2], data[3])
+    for got, r, blocks in zip((gx, genv, gw, gy), rgrads, (t.x_slices, t.env_slices, None, t.env_slices)):
+        assert block_rel_err(got.cpu().numpy(), r, blocks) <= BWD_TOL
+    err = block_rel_err(gpw.cpu().numpy(), t.path_weight_grad(data[0], data[1], renv, data[5]))
+    _note(f"sweep lmax{lmax}{'F' if full else 'N'}U{U}: training grads within {BWD_TOL}, grad_path_w err={err:.2e}")
+    assert err <= BWD_TOL
+
+
 @pytest.mark.parametrize("lmax,full,U", [(2, True, 64), (3, True, 128), (1, False, 16)])
 def test_skewed_degrees(at, lmax, full, U):
     """Heavy-tailed segment lengths: many empty centers, many short ones, a few with
