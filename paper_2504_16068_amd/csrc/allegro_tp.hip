@@ -3,21 +3,29 @@
 // What is computed is stated in include/allegro_tp.h (arxiv 2504.16068, §II.D:
 // the tensor product, its first derivative, and the embedding it consumes).
 //
-// Mapping (wave64, one 64-lane workgroup per center atom):
+// Mapping (wave64; one workgroup of several waves per center atom):
 //   * lane <-> channel u.  With U < 64 a wave holds 64/U lane groups that take
-//     every (64/U)-th edge of the segment; with U = 128 each lane owns two
-//     channels, processed one after the other.
-//   * Path weights W[:, u] and env[n, u, :] are loaded once per center into
-//     VGPRs; every edge then streams x (and g) from HBM and the contraction
-//     runs in registers with the coupling coefficients as instruction
-//     literals (generated cores, tp_cores.inc).
+//     interleaved edges of the segment; with U = 128 the workgroup's waves are
+//     split between the two channel halves.
+//   * The center's slabs (64 consecutive [U][d1] rows, contiguous in HBM) are
+//     dealt to its waves; each slab moves through an LDS tile with 16-byte
+//     coalesced accesses and each lane then works on its own row.
+//   * Direct kernels (every lmax; the lmax-3 forward and training backward
+//     use the per-center matrices below): path weights W[:, u] and
+//     env[n, u, :] are loaded once per center into VGPRs and the contraction
+//     runs in registers with the coupling coefficients as instruction literals
+//     (generated cores, tp_cores.inc).
+//   * Per-center matrices at lmax 3: the forward as out = M x and grad_x as
+//     M^T g with M built once per center, and the training backward's
+//     segment sums from the per-center products G = sum_e x g^T, their rows
+//     split over 8 waves (generated TPMFwd, TPMBwdX, TPGEnv).
 //   * Segment ownership: a center's workgroup owns its env / grad_env rows, so
-//     every segmented reduction is a fixed-order register accumulation -- no
-//     atomics, bit-identical from run to run.
-//   * The embedding VJP (grad_w, grad_Y) reruns the segment with lane <-> edge:
-//     grad_env of the center is staged in LDS and read as wave-uniform
-//     broadcasts, so the sum over channels for grad_Y needs no cross-lane
-//     reduction.
+//     every segmented reduction is a fixed-order sum (registers, then the
+//     waves' parts in LDS in wave order) -- no atomics, bit-identical from run
+//     to run.
+//   * The embedding VJP (grad_w, grad_Y) runs after grad_env is complete, in
+//     batches of 8 edges staged in LDS: grad_w lane-per-channel, grad_Y with 8
+//     lanes per edge and an xor butterfly over them.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
