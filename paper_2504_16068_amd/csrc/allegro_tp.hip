@@ -50,6 +50,10 @@ using namespace allegro_dev;
 
 constexpr int kWave = 64;
 
+// Row stride (floats) for per-lane rows of n floats written to LDS by the 64
+// lanes of a wave at once: odd, so that the lanes' rows start in distinct banks.
+constexpr int odd_stride(int n) { return n | 1; }
+
 template <int U>
 struct Lanes {
   static_assert(U == 16 || U == 32 || U == 64 || U == 128, "U must be 16, 32, 64 or 128");
@@ -509,10 +513,11 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
   constexpr int PER = (TF4 + NT - 1) / NT;
   constexpr int TILE = T * kWave * RS;      // floats of one staged tile
   constexpr int EB = 8, WROW = U + 1, STAGE = EB * (WROW + D2);
-  constexpr int GE_ROW = U * D2, GE_PART = NW * kWave * D2;
-  constexpr int PC = NP < 2 * TILE / (NW * kWave) ? NP : 2 * TILE / (NW * kWave);  // paths per reduction chunk
+  constexpr int GS = odd_stride(D2), GE_ROW = U * D2, GE_PART = NW * kWave * GS;
+  constexpr int PC_FIT = (2 * TILE / (NW * kWave) - 1) | 1;
+  constexpr int PC = NP < PC_FIT ? NP : PC_FIT, PS = odd_stride(PC);  // paths per reduction chunk, their stride
   constexpr int R1 = 2 * TILE > GE_PART ? 2 * TILE : GE_PART;
-  constexpr int R2 = NW * STAGE > NW * kWave * PC ? NW * STAGE : NW * kWave * PC;
+  constexpr int R2 = NW * STAGE > NW * kWave * PS ? NW * STAGE : NW * kWave * PS;
   constexpr int REST = R1 > R2 ? R1 : R2;
   constexpr int LPE = L::LPE, ES = D2 + 1;  // env rows padded to D2 + 1 floats (distinct banks)
   constexpr int ENV = LPE * ES;
@@ -642,14 +647,14 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       wr.load(path_w, U, ul + t * kWave);
       GE::finish_ge(wave, wr, G, ge);
 #pragma unroll
-      for (int j = 0; j < D2; ++j) rest[(wave * kWave + lane) * D2 + j] = ge[j];
+      for (int j = 0; j < D2; ++j) rest[(wave * kWave + lane) * GS + j] = ge[j];
     }
     lds_sync<NW>();
     for (int i = tid; i < L::LPE * D2; i += NT) {
       const int uw = i / D2, j = i % D2;
       float a = 0.0f;
       for (int k = 0; k < NW; ++k)
-        for (int q = 0; q < L::G; ++q) a += rest[((k * kWave) + q * L::LPE + uw) * D2 + j];
+        for (int q = 0; q < L::G; ++q) a += rest[((k * kWave) + q * L::LPE + uw) * GS + j];
       ge_l[(uw + t * kWave) * D2 + j] = a;
       grad_env[(n * U + uw + t * kWave) * D2 + j] = a;
     }
@@ -674,13 +679,13 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       constexpr int p0 = decltype(ic)::value * PC, pn = NP - p0 < PC ? NP - p0 : PC;
       if (grp == 0) {
 #pragma unroll
-        for (int q = 0; q < pn; ++q) rest[(wave * kWave + ul) * PC + q] = gw[p0 + q];
+        for (int q = 0; q < pn; ++q) rest[(wave * kWave + ul) * PS + q] = gw[p0 + q];
       }
       lds_sync<NW>();
       for (int i = tid; i < L::LPE * pn; i += NT) {
         const int q = i / L::LPE, uw = i % L::LPE;
         float a = 0.0f;
-        for (int k = 0; k < NW; ++k) a += rest[(k * kWave + uw) * PC + q];
+        for (int k = 0; k < NW; ++k) a += rest[(k * kWave + uw) * PS + q];
         pw_part[(n * NP + p0 + q) * U + uw + t * kWave] = a;
       }
       lds_sync<NW>();
@@ -799,13 +804,15 @@ struct BwdLds {
   static constexpr int EB = 8;          // edges per pass-2 batch of one wave (8 lanes per edge)
   static constexpr int WROW = U + 1;    // padded w row: per-lane row reads hit distinct banks
   static constexpr int P1 = NW * 2 * TILE_F4 * 4;
-  static constexpr int GE_PART = NW * kWave * D2;
+  static constexpr int GS = odd_stride(D2);  // row stride of the grad_env partial sums
+  static constexpr int GE_PART = NW * kWave * GS;
   static constexpr int GE_ROW = U * D2;
   static constexpr int STAGE = EB * (WROW + D2);
   static constexpr int P2 = GE_PART + GE_ROW + NW * STAGE;
-  static constexpr int PC_FIT = P1 / (NW * kWave);
+  static constexpr int PC_FIT = (P1 / (NW * kWave) - 1) | 1;  // odd, and its stride fits in P1
   static constexpr int PC = WG ? (NP < PC_FIT ? NP : PC_FIT) : 1;  // paths per reduction chunk
-  static constexpr int SW = WG ? NW * kWave * PC : 0;
+  static constexpr int PS = odd_stride(PC);                        // their row stride
+  static constexpr int SW = WG ? NW * kWave * PS : 0;
   static constexpr int FLOATS = P1 > P2 ? (P1 > SW ? P1 : SW) : (P2 > SW ? P2 : SW);
   static_assert(!WG || PC >= 1, "LDS too small for the path-weight partial sums");
 };
@@ -856,13 +863,13 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
       constexpr int p0 = decltype(ic)::value * B::PC, pn = NP - p0 < B::PC ? NP - p0 : B::PC;
       if (grp == 0) {
 #pragma unroll
-        for (int q = 0; q < pn; ++q) lds[(wave * kWave + ul) * B::PC + q] = sw[p0 + q];
+        for (int q = 0; q < pn; ++q) lds[(wave * kWave + ul) * B::PS + q] = sw[p0 + q];
       }
       lds_sync<NW>();
       for (int i = tid; i < U * pn; i += NT) {
         const int q = i / U, uu = i % U, tt = uu / kWave, uw = uu % L::LPE;
         float a = 0.0f;
-        for (int k = 0; k < WPT; ++k) a += lds[((tt * WPT + k) * kWave + uw) * B::PC + q];
+        for (int k = 0; k < WPT; ++k) a += lds[((tt * WPT + k) * kWave + uw) * B::PS + q];
         pw_part[(n * NP + p0 + q) * U + uu] = a;
       }
       lds_sync<NW>();
@@ -872,13 +879,13 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   // grad_env: the waves' and lane groups' partial sums, in a fixed order
   float *ge_part = lds, *ge_l = lds + B::GE_PART;
 #pragma unroll
-  for (int j = 0; j < D2; ++j) ge_part[(wave * kWave + lane) * D2 + j] = ge[j];
+  for (int j = 0; j < D2; ++j) ge_part[(wave * kWave + lane) * B::GS + j] = ge[j];
   lds_sync<NW>();
   for (int i = tid; i < U * D2; i += NT) {
     const int uu = i / D2, j = i % D2, tt = uu / kWave, uw = uu % L::LPE;
     float a = 0.0f;
     for (int k = 0; k < WPT; ++k)
-      for (int q = 0; q < L::G; ++q) a += ge_part[((tt * WPT + k) * kWave + q * L::LPE + uw) * D2 + j];
+      for (int q = 0; q < L::G; ++q) a += ge_part[((tt * WPT + k) * kWave + q * L::LPE + uw) * B::GS + j];
     ge_l[i] = a;
     grad_env[n * U * D2 + i] = a;
   }
