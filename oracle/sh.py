@@ -18,7 +18,11 @@ harmonics are built from their definition:
 
 Parity unpinned for the normalisation and sign conventions (readings); the
 values themselves are pinned by the Cartesian closed forms, scipy's complex
-harmonics, the addition theorem and quadrature orthonormality.
+harmonics, the addition theorem and quadrature orthonormality.  The gradient
+with respect to the edge vector is exact (the derivative of the same
+recurrence); it is pinned by finite differences of the values, closed forms
+for l = 1 and 2, homogeneity and rotation equivariance, and its VJP by
+directional differences of the loss <grad_Y, Y(r)>.
 """
 
 from __future__ import annotations
@@ -35,6 +39,35 @@ def _unit(xyz) -> np.ndarray:
     return v / np.linalg.norm(v, axis=-1, keepdims=True)
 
 
+def _reduced_legendre(l: int, m: int, z):
+    """R_l^m(z) and its derivative dR_l^m/dz, for 0 <= m <= l.
+
+    P_l^m(z) = (1 - z^2)^{m/2} R_l^m(z) with the Condon-Shortley phase:
+        R_m^m = (-1)^m (2m - 1)!!,   R_{m+1}^m = (2m + 1) z R_m^m,
+        (k - m) R_k^m = (2k - 1) z R_{k-1}^m - (k + m - 1) R_{k-2}^m.
+    The derivative follows the same recurrence differentiated term by term:
+        dR_m^m = 0,   dR_{m+1}^m = (2m + 1) R_m^m,
+        (k - m) dR_k^m = (2k - 1) (R_{k-1}^m + z dR_{k-1}^m) - (k + m - 1) dR_{k-2}^m.
+    """
+    double_fact = 1.0
+    for t in range(1, 2 * m, 2):
+        double_fact *= t
+    r_prev = np.full(np.shape(z), (-1.0) ** m * double_fact)
+    d_prev = np.zeros(np.shape(z))
+    if l == m:
+        return r_prev, d_prev
+    r_cur, d_cur = z * (2 * m + 1) * r_prev, (2 * m + 1) * r_prev
+    for k in range(m + 2, l + 1):
+        r_next = ((2 * k - 1) * z * r_cur - (k + m - 1) * r_prev) / (k - m)
+        d_next = ((2 * k - 1) * (r_cur + z * d_cur) - (k + m - 1) * d_prev) / (k - m)
+        r_prev, r_cur, d_prev, d_cur = r_cur, r_next, d_cur, d_next
+    return r_cur, d_cur
+
+
+def _norm(l: int, m: int) -> float:
+    return sqrt((2 * l + 1) / (4 * pi) * factorial(l - m) / factorial(l + m))
+
+
 def sh_complex(l: int, xyz) -> np.ndarray:
     """Orthonormal complex harmonics [n, 2l+1] (m = -l..l) at the directions xyz [n, 3]."""
     v = _unit(xyz)
@@ -42,23 +75,37 @@ def sh_complex(l: int, xyz) -> np.ndarray:
     n = v.shape[:-1]
     out = np.zeros(n + (2 * l + 1,), dtype=complex)
     for m in range(0, l + 1):
-        # reduced associated Legendre R_k^m(z), P_k^m = (1-z^2)^{m/2} R_k^m, CS phase included
-        double_fact = 1.0
-        for t in range(1, 2 * m, 2):
-            double_fact *= t
-        r_prev = np.full(n, (-1.0) ** m * double_fact)  # R_m^m
-        if l == m:
-            r_l = r_prev
-        else:
-            r_cur = z * (2 * m + 1) * r_prev  # R_{m+1}^m
-            for k in range(m + 2, l + 1):
-                r_prev, r_cur = r_cur, ((2 * k - 1) * z * r_cur - (k + m - 1) * r_prev) / (k - m)
-            r_l = r_cur
-        norm = sqrt((2 * l + 1) / (4 * pi) * factorial(l - m) / factorial(l + m))
-        ym = norm * r_l * (x + 1j * y) ** m
+        r_l, _ = _reduced_legendre(l, m, z)
+        ym = _norm(l, m) * r_l * (x + 1j * y) ** m
         out[..., l + m] = ym
         if m > 0:
             out[..., l - m] = (-1) ** m * np.conj(ym)
+    return out
+
+
+def sh_complex_grad_u(l: int, u) -> np.ndarray:
+    """Gradient of the complex harmonics' polynomial form in the unit vector, [n, 2l+1, 3].
+
+    For m >= 0, Y_l^m = N R_l^m(u_z) (u_x + i u_y)^m is a polynomial in the
+    components of u; its partial derivatives (the components taken as
+    independent variables) are
+        d/du_x = N R (m (u_x + i u_y)^{m-1}),  d/du_y = i d/du_x,
+        d/du_z = N (dR/dz) (u_x + i u_y)^m,
+    and Y_l^{-m} = (-1)^m conj(Y_l^m) gives the negative orders.  Only the part
+    tangent to the sphere survives the chain rule through u = r/|r|.
+    """
+    v = np.asarray(u, dtype=np.float64)
+    x, y, z = v[..., 0], v[..., 1], v[..., 2]
+    out = np.zeros(v.shape[:-1] + (2 * l + 1, 3), dtype=complex)
+    w = x + 1j * y
+    for m in range(0, l + 1):
+        r_l, dr_l = _reduced_legendre(l, m, z)
+        nm = _norm(l, m)
+        dw = m * w ** (m - 1) if m > 0 else np.zeros_like(w)
+        col = np.stack([nm * r_l * dw, 1j * nm * r_l * dw, nm * dr_l * w ** m], axis=-1)
+        out[..., l + m, :] = col
+        if m > 0:
+            out[..., l - m, :] = (-1) ** m * np.conj(col)
     return out
 
 
@@ -75,26 +122,28 @@ def sh_real_all(lmax: int, xyz) -> np.ndarray:
     return np.concatenate([sh_real(l, xyz) for l in range(lmax + 1)], axis=-1)
 
 
-def sh_real_all_grad(lmax: int, vec, h: float = 1e-4) -> np.ndarray:
+def sh_real_all_grad(lmax: int, vec) -> np.ndarray:
     """d Y_j / d vec for the concatenated real harmonics, shape [n, (lmax+1)^2, 3].
 
-    Y depends on the direction only (Y(s r) = Y(r) for s > 0), and is evaluated
-    on the vector itself (not its unit vector), so this is the gradient with
-    respect to the edge vector r_ij.  Fourth-order central differences in fp64,
-    with the step scaled by |r|:
-        f'(r) = (-f(r + 2h) + 8 f(r + h) - 8 f(r - h) + f(r - 2h)) / (12 h).
-    Truncation error O(h^4) and rounding O(eps / h) are both far below 1e-9
-    relative for |r| of order 1.
+    Y depends on the direction only (Y(s r) = Y(r) for s > 0) and is evaluated
+    on the edge vector r_ij itself, so this is the gradient with respect to the
+    edge vector.  Exact (fp64): the gradient of the polynomial form in the unit
+    vector (``sh_complex_grad_u``, from the derivative of the Legendre
+    recurrence and the product rule on (u_x + i u_y)^m), chained through
+    du/dr = (I - u u^T)/|r|, then moved to the real basis by the same Q_l and
+    scaled like the values (component normalisation).
     """
     v = np.asarray(vec, dtype=np.float64)
-    scale = np.linalg.norm(v, axis=-1, keepdims=True)
-    out = np.zeros(v.shape[:-1] + ((lmax + 1) ** 2, 3))
-    for k in range(3):
-        step = np.zeros_like(v)
-        step[..., k] = h * scale[..., 0]
-        f = [sh_real_all(lmax, v + c * step) for c in (2, 1, -1, -2)]
-        out[..., k] = (-f[0] + 8 * f[1] - 8 * f[2] + f[3]) / (12 * h * scale)
-    return out
+    r = np.linalg.norm(v, axis=-1)
+    u = v / r[..., None]
+    proj = (np.eye(3) - u[..., :, None] * u[..., None, :]) / r[..., None, None]
+    blocks = []
+    for l in range(lmax + 1):
+        jc = np.einsum("...mk,...kq->...mq", sh_complex_grad_u(l, u), proj)
+        jr = np.einsum("am,...mq->...aq", real_basis_change(l), jc)
+        assert np.abs(jr.imag).max(initial=0.0) < 1e-10 * max(1.0, np.abs(jr.real).max(initial=0.0))
+        blocks.append(jr.real * sqrt(4 * pi))
+    return np.concatenate(blocks, axis=-2)
 
 
 def sh_backward(lmax: int, vec, grad_y) -> np.ndarray:

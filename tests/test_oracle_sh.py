@@ -82,23 +82,60 @@ def test_wigner_properties():
     np.testing.assert_allclose(wigner.wigner_d_real(1, r1), perm @ r1 @ perm.T, atol=1e-12)
 
 
-def test_gradient_closed_form_l1_and_scale_invariance():
+def _fd_grad(lmax, v, h=1e-4):
+    """Fourth-order central differences of the values, step scaled by |r| (a pin of the
+    exact gradient: truncation O(h^4) and rounding O(eps/h) stay near 1e-11 relative)."""
+    scale = np.linalg.norm(v, axis=-1, keepdims=True)
+    out = np.zeros(v.shape[:-1] + ((lmax + 1) ** 2, 3))
+    for k in range(3):
+        step = np.zeros_like(v)
+        step[..., k] = h * scale[..., 0]
+        f = [sh.sh_real_all(lmax, v + c * step) for c in (2, 1, -1, -2)]
+        out[..., k] = (-f[0] + 8 * f[1] - 8 * f[2] + f[3]) / (12 * h * scale)
+    return out
+
+
+def _vectors(n, seed):
+    rng = np.random.default_rng(seed)
+    v = rng.standard_normal((n, 3)) * rng.uniform(0.3, 6.0, (n, 1))
+    special = np.array([[0, 0, 1.5], [0, 0, -2.0], [1, 0, 0], [0, -1, 0], [1e-7, 0, 1], [1e-3, 2e-3, 1e-3]])
+    return np.concatenate([special, v])
+
+
+def test_gradient_matches_finite_differences():
+    v = _vectors(60, 8)
+    for lmax in (1, 2, 3, 4):
+        exact = sh.sh_real_all_grad(lmax, v)
+        fd = _fd_grad(lmax, v)
+        scale = np.abs(exact).max(axis=(1, 2), keepdims=True)
+        assert np.max(np.abs(exact - fd) / scale) < 1e-9, lmax
+
+
+def test_gradient_closed_forms_l1_l2():
     rng = np.random.default_rng(4)
     v = rng.standard_normal((30, 3)) * rng.uniform(0.5, 5.0, (30, 1))
     grad = sh.sh_real_all_grad(2, v)
     r = np.linalg.norm(v, axis=1)
     u = v / r[:, None]
-    # l = 1: Y = sqrt3 (y, z, x) / |r|  ->  dY/dr = sqrt3 (e_a - u_a u) / |r|
+    eye = np.eye(3)
+    # du_a/dr = (e_a - u_a u) / |r|
+    du = [(eye[a][None, :] - u[:, a:a + 1] * u) / r[:, None] for a in range(3)]
+    # l = 1: Y = sqrt3 (u_y, u_z, u_x)
     for col, axis in ((1, 1), (2, 2), (3, 0)):
-        expect = sqrt(3) * (np.eye(3)[axis][None, :] - u[:, axis:axis + 1] * u) / r[:, None]
-        np.testing.assert_allclose(grad[:, col, :], expect, atol=1e-9)
-    # Y is homogeneous of degree 0, so r . grad Y = 0 for every component
-    np.testing.assert_allclose(np.einsum("ek,ejk->ej", v, grad), 0.0, atol=1e-9)
-    # the scalar component is constant
-    np.testing.assert_allclose(grad[:, 0, :], 0.0, atol=1e-12)
+        np.testing.assert_allclose(grad[:, col, :], sqrt(3) * du[axis], atol=1e-13)
+    # l = 2: sqrt15 u_x u_y, sqrt15 u_y u_z, sqrt5/2 (3 u_z^2 - 1), sqrt15 u_x u_z, sqrt15/2 (u_x^2 - u_y^2)
+    x, y, z = (u[:, a:a + 1] for a in range(3))
+    expect = [sqrt(15) * (y * du[0] + x * du[1]), sqrt(15) * (z * du[1] + y * du[2]), sqrt(5) / 2 * 6 * z * du[2],
+              sqrt(15) * (z * du[0] + x * du[2]), sqrt(15) / 2 * (2 * x * du[0] - 2 * y * du[1])]
+    for c, e in enumerate(expect):
+        np.testing.assert_allclose(grad[:, 4 + c, :], e, atol=1e-13)
+    # Y is homogeneous of degree 0, so r . grad Y = 0 for every component; Y_0 is constant
+    grad3 = sh.sh_real_all_grad(4, v)
+    np.testing.assert_allclose(np.einsum("ek,ejk->ej", v, grad3), 0.0, atol=1e-13)
+    np.testing.assert_allclose(grad3[:, 0, :], 0.0, atol=0.0)
 
 
-def test_gradient_equivariance_and_vjp():
+def test_gradient_equivariance():
     rng = np.random.default_rng(5)
     rot = wigner.random_rotation(rng)
     v = rng.standard_normal((20, 3))
@@ -108,6 +145,21 @@ def test_gradient_equivariance_and_vjp():
     d = wigner.wigner_d_blocks(blocks, rot)
     j_rot = sh.sh_real_all_grad(lmax, v @ rot.T)
     j = sh.sh_real_all_grad(lmax, v)
-    np.testing.assert_allclose(np.einsum("ejk,kl->ejl", j_rot, rot), np.einsum("ij,ejk->eik", d, j), atol=1e-8)
-    gy = rng.standard_normal((20, 16))
-    np.testing.assert_allclose(sh.sh_backward(lmax, v, gy), np.einsum("ej,ejk->ek", gy, j), atol=1e-12)
+    np.testing.assert_allclose(np.einsum("ejk,kl->ejl", j_rot, rot), np.einsum("ij,ejk->eik", d, j), atol=1e-10)
+
+
+def test_backward_directional_differences():
+    """sh_backward against the loss L(r) = <grad_Y, Y(r)> alone: for a random direction d
+    per edge, <grad_vec, d> equals dL(r + t d)/dt at t = 0 (fourth-order differences
+    of the values; no Jacobian involved)."""
+    rng = np.random.default_rng(6)
+    v = _vectors(200, 9)
+    for lmax in (1, 2, 3):
+        gy = rng.standard_normal((len(v), (lmax + 1) ** 2))
+        d = rng.standard_normal(v.shape)
+        h = 1e-4 * np.linalg.norm(v, axis=1, keepdims=True)
+        loss = [np.sum(gy * sh.sh_real_all(lmax, v + c * h * d), axis=1) for c in (2, 1, -1, -2)]
+        fd = (-loss[0] + 8 * loss[1] - 8 * loss[2] + loss[3]) / (12 * h[:, 0])
+        got = np.sum(sh.sh_backward(lmax, v, gy) * d, axis=1)
+        scale = np.linalg.norm(gy, axis=1) * np.linalg.norm(d, axis=1) / np.linalg.norm(v, axis=1)
+        assert np.max(np.abs(got - fd) / scale) < 1e-9, lmax
