@@ -158,6 +158,31 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
                               float *grad_path_w, void *workspace, size_t workspace_bytes,
                               void *stream);
 
+/* Allocation-free training backward, for callers that cannot allocate device
+ * memory or pass a workspace (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): the same outputs as
+ * allegro_tp_backward_train, with the path-weight partial sums kept in a
+ * static device array of the library instead of a workspace.  The array is
+ * 64 MiB of fp32 (16 Mi floats) and is held by every GPU the library runs on
+ * until the process ends.  The centers are processed in chunks of
+ * C = floor(16 Mi / (n_paths * U)) - 384 centers (1,543 at lmax 3, U = 128;
+ * 8,354 at lmax 2, U = 64); each chunk's per-center rows are summed in a fixed
+ * order into one row, and the chunk rows in order into grad_path_w, so the
+ * result is deterministic and equals allegro_tp_backward_train's up to fp32
+ * rounding order (grad_x, grad_env, grad_w and grad_Y are bit-identical to
+ * it).  At most 256 chunks: N > 256 * C returns ALLEGRO_E_INVALID before any
+ * launch.  Every call on one GPU shares that GPU's array and overwrites it, so
+ * calls that overlap on one GPU (several streams or threads) race and must be
+ * serialised by the caller.  The call itself allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); the first call on a device looks the
+ * array's address up there (hipGetSymbolAddress).  Errors as for
+ * allegro_tp_backward_train. */
+int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
+                                      const float *x, const float *env, const float *path_w,
+                                      const float *grad_out, const float *w, const float *Y,
+                                      float *grad_x, float *grad_env, float *grad_w, float *grad_Y,
+                                      float *grad_path_w, void *stream);
+
 /* Real spherical harmonics of the edge vectors, the embedding input of the
  * environment sum (Appendix "Mixed-Precision Architecture": embedded in fp64,
  * then cast to fp32): Y[E][d2] = fl32(Y^l_m(vec_e)), l = 0..lmax, m = -l..l,

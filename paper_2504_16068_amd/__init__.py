@@ -26,6 +26,7 @@ from .binding import (  # noqa: F401
     allegro_sh_forward,
     allegro_tp_backward,
     allegro_tp_backward_train,
+    allegro_tp_backward_train_noalloc,
     allegro_tp_backward_workspace,
     allegro_tp_forward,
     allegro_tp_plan_create,

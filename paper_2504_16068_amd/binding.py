@@ -28,7 +28,7 @@ ALLEGRO_VALIDATE = 4
 EXPORTED = (
     "allegro_tp_plan_create", "allegro_tp_plan_destroy", "allegro_tp_plan_query", "allegro_tp_plan_cg",
     "allegro_env_embed", "allegro_tp_forward", "allegro_tp_backward", "allegro_tp_backward_workspace",
-    "allegro_tp_backward_train", "allegro_sh_forward", "allegro_sh_backward",
+    "allegro_tp_backward_train", "allegro_tp_backward_train_noalloc", "allegro_sh_forward", "allegro_sh_backward",
     "allegro_layer_buffers", "allegro_layer_forward", "allegro_layer_backward",
     "allegro_last_error",
 )
@@ -63,6 +63,7 @@ def _load() -> ctypes.CDLL:
     lib.allegro_tp_backward.argtypes = [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.allegro_tp_backward_workspace.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_size_t)]
     lib.allegro_tp_backward_train.argtypes = [vp, i64, i64] + [vp] * 13 + [ctypes.c_size_t, vp]
+    lib.allegro_tp_backward_train_noalloc.argtypes = [vp, i64, i64] + [vp] * 13
     lib.allegro_sh_forward.argtypes = [vp, i64, vp, vp, vp]
     lib.allegro_sh_backward.argtypes = [vp, i64, vp, vp, vp, vp]
     szp = ctypes.POINTER(ctypes.c_size_t)
@@ -270,6 +271,34 @@ def allegro_tp_backward_train(plan: Plan, row_ptr, x, env, path_w, grad_out, w, 
                                           _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw),
                                           _ptr(gy), _ptr(gpw), _ptr(workspace),
                                           workspace.numel() * workspace.element_size(), _stream(stream, dev)))
+    return gx, genv, gw, gy, gpw
+
+
+def allegro_tp_backward_train_noalloc(plan: Plan, row_ptr, x, env, path_w, grad_out, w, Y, outs=None, stream=None):
+    """Returns (grad_x, grad_env, grad_w, grad_Y, grad_path_w); the library keeps the
+    partial sums in its own static device memory (no workspace)."""
+    import torch
+
+    dev = row_ptr.device
+    n, e = _sizes(plan, row_ptr, x.shape[0])
+    _need(x, "x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(env, "env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(path_w, "path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    _need(grad_out, "grad_out", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(w, "w", (e, plan.U), torch.float32, dev)
+    _need(Y, "Y", (e, plan.d2), torch.float32, dev)
+    if outs is None:
+        outs = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(Y),
+                torch.empty_like(path_w))
+    gx, genv, gw, gy, gpw = outs
+    _need(gx, "grad_x", (e, plan.U, plan.d1), torch.float32, dev)
+    _need(genv, "grad_env", (n, plan.U, plan.d2), torch.float32, dev)
+    _need(gw, "grad_w", (e, plan.U), torch.float32, dev)
+    _need(gy, "grad_Y", (e, plan.d2), torch.float32, dev)
+    _need(gpw, "grad_path_w", (plan.n_paths, plan.U), torch.float32, dev)
+    _check(_lib.allegro_tp_backward_train_noalloc(plan.handle, n, e, _ptr(row_ptr), _ptr(x), _ptr(env), _ptr(path_w),
+                                                  _ptr(grad_out), _ptr(w), _ptr(Y), _ptr(gx), _ptr(genv), _ptr(gw),
+                                                  _ptr(gy), _ptr(gpw), _stream(stream, dev)))
     return gx, genv, gw, gy, gpw
 
 

@@ -1082,12 +1082,12 @@ __global__ __launch_bounds__(256) void pw_reduce_rows_kernel(int64_t N, int cols
   chunk_sums[int64_t(blockIdx.y) * cols + c] = (a0 + a1) + (a2 + a3);
 }
 
-__global__ __launch_bounds__(256) void pw_reduce_chunks_kernel(int cols, const float *__restrict__ chunk_sums,
+__global__ __launch_bounds__(256) void pw_reduce_chunks_kernel(int rows, int cols, const float *__restrict__ chunk_sums,
                                                                float *__restrict__ grad_pw) {
   const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
   if (c >= cols) return;
   float a = 0.0f;
-  for (int r = 0; r < kPwChunks; ++r) a += chunk_sums[r * cols + c];
+  for (int r = 0; r < rows; ++r) a += chunk_sums[int64_t(r) * cols + c];
   grad_pw[c] = a;
 }
 
@@ -1096,8 +1096,48 @@ __global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restri
   if (i < n) p[i] = 0.0f;
 }
 
+// ------------------------------------------- allocation-free training backward
+// The path-weight partial sums of allegro_tp_backward_train_noalloc live in a
+// file-scope device array instead of a caller workspace: kNoAllocFloats fp32
+// (64 MiB), held by every GPU the library runs on until the process ends.
+constexpr int64_t kNoAllocFloats = int64_t(16) << 20;
+constexpr int64_t kNoAllocChunks = 256;  // chunk rows kept for the last sum
+static __device__ __align__(256) float scratch[kNoAllocFloats];
+
 // ------------------------------------------------------------- host side
 using allegro_internal::fail;
+
+struct NoAllocLayout {
+  int64_t centers;  // centers per chunk
+};
+
+// rows of cols floats: [centers][cols] per-center sums, [128][cols] range sums,
+// [kNoAllocChunks][cols] chunk sums
+NoAllocLayout noalloc_layout(int cols) {
+  const int64_t rows = kNoAllocFloats / cols;
+  return {rows - kPwChunks - kNoAllocChunks};
+}
+
+// Device address of `scratch` on the current device, looked up once per device
+// (each GPU holds its own copy of the array at its own address).
+int noalloc_scratch(float **out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static float *addr[kMaxDevices] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(ALLEGRO_E_HIP, "no current HIP device for the static scratch (device %d)", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    const hipError_t err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || !p)
+      return fail(ALLEGRO_E_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(err));
+    addr[dev] = static_cast<float *>(p);
+  }
+  *out = addr[dev];
+  return ALLEGRO_OK;
+}
 
 bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
@@ -1395,8 +1435,62 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
   if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
   const unsigned cb = unsigned((cols + 255) / 256);
   hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
-  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, cols, chunks, grad_path_w);
+  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w);
   return after_launch("allegro_tp_backward_train");
+}
+
+int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
+                                      const float *x, const float *env, const float *path_w, const float *grad_out,
+                                      const float *w, const float *Y, float *grad_x, float *grad_env, float *grad_w,
+                                      float *grad_Y, float *grad_path_w, void *stream) {
+  int rc = check_sizes(plan, N, E, row_ptr);
+  if (rc) return rc;
+  if ((rc = check_tensor(grad_path_w, "grad_path_w"))) return rc;
+  const int cols = int(plan->table.paths.size()) * plan->U;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (N == 0) {  // no centers, no edges: the gradient is zero
+    hipLaunchKernelGGL(zero_floats_kernel, dim3(unsigned((cols + 255) / 256)), dim3(256), 0, s, cols, grad_path_w);
+    return after_launch("allegro_tp_backward_train_noalloc");
+  }
+  const NoAllocLayout lay = noalloc_layout(cols);
+  const int64_t n_chunks = (N + lay.centers - 1) / lay.centers;
+  if (lay.centers < 1 || n_chunks > kNoAllocChunks)
+    return fail(ALLEGRO_E_INVALID,
+                "N=%lld centers exceed the allocation-free maximum of %lld for this plan (%d path-weight columns, "
+                "%zu-byte static scratch)", (long long)N, (long long)lay.centers * kNoAllocChunks, cols,
+                sizeof(float) * kNoAllocFloats);
+  if ((rc = check_tensor(grad_env, "grad_env")) || (rc = check_tensor(env, "env")) ||
+      (rc = check_tensor(path_w, "path_w")))
+    return rc;
+  if (E > 0 && ((rc = check_tensor(x, "x")) || (rc = check_tensor(grad_out, "grad_out")) ||
+                (rc = check_tensor(w, "w")) || (rc = check_tensor(Y, "Y")) || (rc = check_tensor(grad_x, "grad_x")) ||
+                (rc = check_tensor(grad_w, "grad_w")) || (rc = check_tensor(grad_Y, "grad_Y"))))
+    return rc;
+  float *scr = nullptr;
+  if ((rc = noalloc_scratch(&scr))) return rc;
+  auto *mp = const_cast<allegro_tp_plan *>(plan);
+  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const Kernels k = select(plan);
+  if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  // scratch: per-center rows of one chunk, the 128 range sums of a chunk, then
+  // one row per chunk; every region is fully written before it is read
+  float *part = scr, *ranges = part + lay.centers * cols, *chunk_rows = ranges + int64_t(kPwChunks) * cols;
+  const int64_t ud2 = int64_t(plan->U) * plan->table.d2;
+  const unsigned cb = unsigned((cols + 255) / 256);
+  for (int64_t c = 0; c < n_chunks; ++c) {
+    const int64_t n0 = c * lay.centers, n1 = std::min(N, n0 + lay.centers);
+    // the chunk's centers as a CSR of their own: row_ptr values stay absolute
+    // edge indices, center-indexed tensors are offset to the chunk's first center
+    k.bwd_wg(dim3(unsigned(n1 - n0)), s, row_ptr + n0, x, env + n0 * ud2, path_w, grad_out, w, Y, grad_x,
+             grad_env + n0 * ud2, grad_w, grad_Y, part);
+    hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, n1 - n0, cols, part, ranges);
+    hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, ranges,
+                       chunk_rows + c * cols);
+    if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
+  }
+  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, int(n_chunks), cols, chunk_rows,
+                     grad_path_w);
+  return after_launch("allegro_tp_backward_train_noalloc");
 }
 
 // One edge per thread in 256-thread blocks; the grid's x extent stays below 2^31.
