@@ -89,7 +89,11 @@ enum {
 /* Create a plan for maximum rotation order lmax (1, 2 or 3), U channels
  * (16, 32, 64 or 128) and flags (ALLEGRO_*).  Builds the sparse coupling table
  * on the host; only with ALLEGRO_VALIDATE does it touch the GPU, to allocate
- * the plan's 4-byte device status word.  *plan is set to NULL on failure. */
+ * the plan's 4-byte device status word.  *plan is set to NULL on failure; a
+ * failed allocation returns ALLEGRO_E_NOMEM.  For tests of that path, the
+ * environment variable ALLEGRO_SIMULATE_ALLOC_FAILURE set to "plan", "table"
+ * or "status" makes that allocation fail (the status word's without calling
+ * HIP). */
 int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags);
 
 /* Release a plan (NULL is accepted). The caller must ensure no call using it

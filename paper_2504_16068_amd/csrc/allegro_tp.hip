@@ -10,15 +10,16 @@
 //   * The center's slabs (64 consecutive [U][d1] rows, contiguous in HBM) are
 //     dealt to its waves; each slab moves through an LDS tile with 16-byte
 //     coalesced accesses and each lane then works on its own row.
-//   * Direct kernels (every lmax; the lmax-3 forward and training backward
-//     use the per-center matrices below): path weights W[:, u] and
+//   * Direct kernels (forward at lmax <= 2, inference backward at every
+//     lmax, training backward at lmax <= 2): path weights W[:, u] and
 //     env[n, u, :] are loaded once per center into VGPRs and the contraction
 //     runs in registers with the coupling coefficients as instruction literals
 //     (generated cores, tp_cores.inc).
-//   * Per-center matrices at lmax 3: the forward as out = M x and grad_x as
-//     M^T g with M built once per center, and the training backward's
-//     segment sums from the per-center products G = sum_e x g^T, their rows
-//     split over 8 waves (generated TPMFwd, TPMBwdX, TPGEnv).
+//   * Per-center matrices at lmax 3: the forward as out = M x with M built
+//     once per center, its rows split over 8 waves (generated TPMFwd); the
+//     training backward as grad_x = g M and the per-center products
+//     G = sum_e g^T x on the matrix cores (tp_mfma_bwd_kernel, lane tables
+//     TPMfmaTab), then the embedding VJP in a launch of its own.
 //   * Segment ownership: a center's workgroup owns its env / grad_env rows, so
 //     every segmented reduction is a fixed-order sum (registers, then the
 //     waves' parts in LDS in wave order) -- no atomics, bit-identical from run
@@ -31,6 +32,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -310,14 +312,12 @@ struct KernelTraits {
 // LDS tile.  With many waves on one center the concurrently streamed HBM
 // regions are few and contiguous: a standalone probe of the forward's access
 // pattern measured 4.98 TB/s with one wave per center and 5.51 TB/s with 16.
-// That pays where the kernel is HBM-bound (lmax <= 2, and the lmax-3
-// backward at 128 channels).  Where it is bound by VALU issue (the lmax-3
-// backward at 64 channels), fewer waves per center leave room for more
-// workgroups per compute unit, which overlap one center's reduction phases
-// with another's streaming.  The counts are the fastest of 1, 2, 4, 8 and 16
-// measured for each kernel on the MI355X.  (At lmax 3 the forward and the
-// training backward are tp_matrix_kernel and tp_backward_g_kernel, whose 8
-// waves split the rows of per-center matrices.)
+// That pays where the kernel is HBM-bound (lmax <= 2).  The training backward,
+// which also holds the path-weight sums, is bound by VALU issue; with fewer
+// waves per center more workgroups fit on a compute unit and overlap one
+// center's reduction phases with another's streaming.  The counts are the
+// fastest of 1, 2, 4, 8 and 16 measured for each kernel on the MI355X.  (At
+// lmax 3 the forward is tp_matrix_kernel and the backward tp_mfma_bwd_kernel.)
 template <class Core, int U>
 struct TPWaves {
   static constexpr bool kHigh = Core::LMAX >= 3, kWide = U > 64;
@@ -382,8 +382,7 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 template <class Core>
 constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 
-// MF is the generated matrix: TPMFwd (out = M x) or TPMBwdX (grad_x = M^T g,
-// the same kernel with g as input and grad_x as output).
+// MF is the generated matrix TPMFwd (out = M x).
 template <class Core, int U, class MF>
 __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_matrix_kernel(
     const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
@@ -478,225 +477,28 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
   }
 }
 
-// ---------------------------------- training backward, lmax 3: segment sums
-// grad_env and the path-weight gradient from the per-center products
-// G[k][i] = sum over the center's edges of x[i] g[k] (generated TPGEnv; rows k
-// split over the 8 waves as in TPMFwd):
-//   grad_env[j] = sum_{(k,i)} sum_p W(p) C_pijk G[k][i],
-//   grad_W[p]   = sum_{(k,i)} sum_j C_pijk env[j] G[k][i].
-// Per edge a wave adds x[i] g[k] into its cells (about 930 FMAs per edge and
-// channel over the 8 waves); at the end of the center each wave adds its part
-// of both sums, and the waves' (and lane groups') parts are added in LDS in a
-// fixed order.  Then the embedding's VJP, as in tp_backward_kernel.  grad_x
-// comes from tp_matrix_kernel with TPMBwdX.  This takes about half the VALU
-// work of the direct training backward at lmax 3.
-// The register file holds one such workgroup per compute unit, so nothing else
-// streams while it is in the center-end phases.  To shorten them, the center's
-// env rows (and, in the second launch, half 0 of grad_env[n]) are staged in
-// LDS behind the first tile's loads, and the first embedding-VJP batch is
-// loaded before the sums are formed.  (Staging the path weights per center as
-// well was slower than reading them from cache at use.)
-// With U = 128 the two channel halves are two launches (HALF = 0, then 1; one
-// launch handling both would spill): the first writes half 0's grad_env, the
-// second reads it back for the embedding's VJP, which it alone performs.
-template <class Core, int U, int HALF>
-__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_backward_g_kernel(
-    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
-    const float *__restrict__ path_w, const float *__restrict__ g, const float *__restrict__ w,
-    const float *__restrict__ Y, float *__restrict__ grad_env, float *__restrict__ grad_w,
-    float *__restrict__ grad_Y, float *__restrict__ pw_part) {
-  using GE = TPGEnv<Core::LMAX, Core::FULL>;
+// ------------------------------------------------- embedding VJP (pass 2)
+// The embedding's VJP for the edges [e0, e1) of center n, given its complete
+// grad_env[n] rows [U][D2] in LDS (ge_l), in batches of EB edges dealt round
+// robin to the NW waves of the center; each wave first stages the batch's w
+// and Y rows in its own LDS area (stage, EB * (U + 1 + D2) floats) with one
+// round of coalesced loads:
+//   grad_w[e,u] = sum_j grad_env[n,u,j] Y[e,j]   lane <-> channel (coalesced stores)
+//   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> (edge k, channel eighth q):
+//                 each lane sums U/8 channels, then an xor butterfly over the 8
+//                 lanes of the edge (operands swapped between partners, so all 8
+//                 hold the same bits)
+template <int U, int D2, int NW, int EB>
+__device__ __forceinline__ void embedding_vjp(const float *ge_l, float *stage, int64_t e0, int64_t e1, int wave,
+                                              int lane, const float *__restrict__ w, const float *__restrict__ Y,
+                                              float *__restrict__ grad_w, float *__restrict__ grad_Y) {
   using L = Lanes<U>;
-  constexpr int D1 = Core::D1, D2 = Core::D2, NP = Core::NP, NW = GE::NW, ROWS = GE::ROWS;
-  constexpr int T = 4;                      // slabs per tile and tensor
-  constexpr int RS = D1 + 4, R4 = D1 / 4, SF4 = TileShape<D1>::SF4, TF4 = T * SF4, NT = NW * kWave;
-  constexpr int PER = (TF4 + NT - 1) / NT;
-  constexpr int TILE = T * kWave * RS;      // floats of one staged tile
-  constexpr int EB = 8, WROW = U + 1, STAGE = EB * (WROW + D2);
-  constexpr int GS = odd_stride(D2), GE_ROW = U * D2, GE_PART = NW * kWave * GS;
-  constexpr int PC_FIT = (2 * TILE / (NW * kWave) - 1) | 1;
-  constexpr int PC = NP < PC_FIT ? NP : PC_FIT, PS = odd_stride(PC);  // paths per reduction chunk, their stride
-  constexpr int R1 = 2 * TILE > GE_PART ? 2 * TILE : GE_PART;
-  constexpr int R2 = NW * STAGE > NW * kWave * PS ? NW * STAGE : NW * kWave * PS;
-  constexpr int REST = R1 > R2 ? R1 : R2;
-  constexpr int LPE = L::LPE, ES = D2 + 1;  // env rows padded to D2 + 1 floats (distinct banks)
-  constexpr int ENV = LPE * ES;
-  constexpr int EF4 = LPE * D2 / 4, GF4 = HALF == 1 ? kWave * D2 / 4 : 0;
-  constexpr int SPER = (EF4 + GF4 + NT - 1) / NT;  // float4 per thread staged at the center's start
-  constexpr bool PASS2 = L::CPL == 1 || HALF == 1;
-  static_assert(D1 % 4 == 0 && D1 == NW * ROWS && ROWS % 2 == 0, "rows of whole float4, split evenly");
-  static_assert(D2 % 4 == 0, "env rows of whole float4");
-  // LDS: this half's env[n] rows [LPE][D2 + 1]; grad_env[n] [U][D2] (kept for
-  // pass 2); then one region reused for the x and g tiles, the path-weight
-  // partial sums, the grad_env partial sums and the pass-2 staging
-  __shared__ float4 smem4[(ENV + GE_ROW + REST + 3) / 4];
-  float *envl = reinterpret_cast<float *>(smem4), *ge_l = envl + ENV, *rest = ge_l + GE_ROW;
-  float *xs = rest, *gs = rest + TILE;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
-  const int64_t n = blockIdx.x;
-  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
-  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
-  auto src = [&](int64_t s0, int f, int t) -> int64_t {
-    const int sl = f / SF4, in = f % SF4;
-    if (s0 + sl >= n_slabs) return -1;
-    if constexpr (U <= kWave) {
-      const int64_t base = Slabs<U>::first_edge(e0, s0) * (U * D1 / 4), end = e1 * (U * D1 / 4);
-      const int64_t q = base + f;
-      return q < end ? q : -1;
-    } else {
-      return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
-    }
-  };
-  static_assert(L::CPL == 1 || L::CPL == 2, "one or two channel halves");
-  // one embedding-VJP batch (EB edges) of this wave in registers: w rows, Y rows
-  constexpr int P2W = (EB * U / 4 + kWave - 1) / kWave, P2Y = (EB * D2 + kWave - 1) / kWave;
-  float4 pv[PASS2 ? P2W : 1];
-  float py[PASS2 ? P2Y : 1];
-  auto p2_fetch = [&](int64_t eb) {
-    const int cnt = int(e1 - eb < EB ? (e1 - eb > 0 ? e1 - eb : 0) : EB);
-    const float4 *w4 = reinterpret_cast<const float4 *>(w);
-#pragma unroll
-    for (int q = 0; q < P2W; ++q) {
-      const int i4 = lane + kWave * q;
-      if (i4 < cnt * (U / 4)) pv[q] = w4[eb * (U / 4) + i4];
-    }
-#pragma unroll
-    for (int q = 0; q < P2Y; ++q) {
-      const int i = lane + kWave * q;
-      if (i < cnt * D2) py[q] = Y[eb * D2 + i];
-    }
-  };
-  {
-    constexpr int t = HALF;
-    float G[GE::MAXM];
-#pragma unroll
-    for (int q = 0; q < GE::MAXM; ++q) G[q] = 0.0f;
-    float4 vx[PER], vg[PER];
-    auto fetch = [&](int64_t s0) {
-      const float4 *x4 = reinterpret_cast<const float4 *>(x), *g4 = reinterpret_cast<const float4 *>(g);
-#pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int f = tid + NT * i;
-        const int64_t q = f < TF4 ? src(s0, f, t) : -1;
-        vx[i] = q >= 0 ? load_stream(x4 + q) : make_float4(0.f, 0.f, 0.f, 0.f);
-        vg[i] = q >= 0 ? load_stream(g4 + q) : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-    };
-    if (n_slabs > 0) fetch(0);
-    {
-      // behind the first tile: this half's env[n] rows and (second launch) half
-      // 0 of grad_env[n]
-      float4 v[SPER];
-      const float4 *env4 = reinterpret_cast<const float4 *>(env + (n * U + t * kWave) * D2);
-      const float4 *ge4 = reinterpret_cast<const float4 *>(grad_env + n * U * D2);
-#pragma unroll
-      for (int i = 0; i < SPER; ++i) {
-        const int f = tid + NT * i;
-        if (f < EF4) v[i] = env4[f];
-        else if (f < EF4 + GF4) v[i] = ge4[f - EF4];
-      }
-#pragma unroll
-      for (int i = 0; i < SPER; ++i) {
-        const int f = tid + NT * i;
-        if (f < EF4) {
-          const int q = 4 * f, c = q / D2, j = q % D2;
-          float *d = envl + c * ES + j;
-          d[0] = v[i].x; d[1] = v[i].y; d[2] = v[i].z; d[3] = v[i].w;
-        } else if (f < EF4 + GF4) {
-          *reinterpret_cast<float4 *>(ge_l + 4 * (f - EF4)) = v[i];
-        }
-      }
-    }
-    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
-#pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int f = tid + NT * i;
-        if (f < TF4) {
-          *reinterpret_cast<float4 *>(xs + (f / R4) * RS + 4 * (f % R4)) = vx[i];
-          *reinterpret_cast<float4 *>(gs + (f / R4) * RS + 4 * (f % R4)) = vg[i];
-        }
-      }
-      if (s0 + T < n_slabs) fetch(s0 + T);
-      lds_sync<NW>();
-      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
-#pragma unroll 1
-      for (int sl = 0; sl < cnt; ++sl) {
-        const int r = sl * kWave + lane;
-        float xr[D1], gr[ROWS];
-#pragma unroll
-        for (int q = 0; q < R4; ++q) {
-          const float4 a = *reinterpret_cast<const float4 *>(xs + r * RS + 4 * q);
-          xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
-        }
-#pragma unroll
-        for (int q = 0; q < ROWS; ++q) gr[q] = gs[r * RS + wave * ROWS + q];
-        GE::accumulate(wave, xr, gr, G);  // rows past the segment hold zeros
-      }
-      lds_sync<NW>();  // the tiles may be refilled (or the region reused)
-    }
-    if (n_slabs == 0) lds_sync<NW>();  // the staged rows are visible
-    // the first embedding-VJP batch of this wave, in flight while the sums form
-    if constexpr (PASS2) p2_fetch(e0 + int64_t(wave) * EB);
-    // grad_env: this wave's part for channel u, then the waves' and lane
-    // groups' parts, in order
-    {
-      float ge[D2];
-#pragma unroll
-      for (int j = 0; j < D2; ++j) ge[j] = 0.0f;
-      CachedWeights wr;
-      wr.load(path_w, U, ul + t * kWave);
-      GE::finish_ge(wave, wr, G, ge);
-#pragma unroll
-      for (int j = 0; j < D2; ++j) rest[(wave * kWave + lane) * GS + j] = ge[j];
-    }
-    lds_sync<NW>();
-    for (int i = tid; i < L::LPE * D2; i += NT) {
-      const int uw = i / D2, j = i % D2;
-      float a = 0.0f;
-      for (int k = 0; k < NW; ++k)
-        for (int q = 0; q < L::G; ++q) a += rest[((k * kWave) + q * L::LPE + uw) * GS + j];
-      ge_l[(uw + t * kWave) * D2 + j] = a;
-      grad_env[(n * U + uw + t * kWave) * D2 + j] = a;
-    }
-    lds_sync<NW>();
-    // grad_W: this wave's part, the lane groups by an xor butterfly (same bits
-    // on every lane of a channel), then the waves in order, PC paths at a time
-    float gw[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) gw[p] = 0.0f;
-    {
-      float er[D2];
-#pragma unroll
-      for (int j = 0; j < D2; ++j) er[j] = envl[ul * ES + j];
-      GE::finish_gw(wave, er, G, gw);
-    }
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-#pragma unroll
-      for (int off = L::LPE; off < kWave; off *= 2) gw[p] += __shfl_xor(gw[p], off);
-    }
-    static_for<0, (NP + PC - 1) / PC>([&](auto ic) {
-      constexpr int p0 = decltype(ic)::value * PC, pn = NP - p0 < PC ? NP - p0 : PC;
-      if (grp == 0) {
-#pragma unroll
-        for (int q = 0; q < pn; ++q) rest[(wave * kWave + ul) * PS + q] = gw[p0 + q];
-      }
-      lds_sync<NW>();
-      for (int i = tid; i < L::LPE * pn; i += NT) {
-        const int q = i / L::LPE, uw = i % L::LPE;
-        float a = 0.0f;
-        for (int k = 0; k < NW; ++k) a += rest[(k * kWave + uw) * PS + q];
-        pw_part[(n * NP + p0 + q) * U + uw + t * kWave] = a;
-      }
-      lds_sync<NW>();
-    });
-  }
-
-  if constexpr (!PASS2) return;  // the second launch does pass 2
-  // Pass 2: the embedding's VJP through grad_env (as in tp_backward_kernel).
-  // (With two halves, half 0 of grad_env[n] was staged at the center's start.)
-  float *wl = rest + wave * STAGE;
+  static_assert(EB == 8, "8 lanes per edge in the grad_Y sums");
+  constexpr int WROW = U + 1;  // padded w row: per-lane row reads hit distinct banks
+  const int grp = lane / L::LPE, ul = lane % L::LPE;
+  float *wl = stage;
   float *yl = wl + EB * WROW;
+  const float4 *w4 = reinterpret_cast<const float4 *>(w);
   float gel[L::CPL][D2];
 #pragma unroll
   for (int c = 0; c < L::CPL; ++c)
@@ -705,21 +507,13 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
   for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
     lds_sync<1>();  // this wave's previous batch is done with its staged rows
-#pragma unroll
-    for (int q = 0; q < P2W; ++q) {
-      const int i4 = lane + kWave * q;
-      if (i4 < cnt * (U / 4)) {
-        const int r = (4 * i4) / U, c = (4 * i4) % U;
-        float *dst = wl + r * WROW + c;
-        dst[0] = pv[q].x; dst[1] = pv[q].y; dst[2] = pv[q].z; dst[3] = pv[q].w;
-      }
+    for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
+      const float4 v = w4[eb * (U / 4) + i4];
+      const int r = (4 * i4) / U, c = (4 * i4) % U;
+      float *dst = wl + r * WROW + c;
+      dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
     }
-#pragma unroll
-    for (int q = 0; q < P2Y; ++q) {
-      const int i = lane + kWave * q;
-      if (i < cnt * D2) yl[i] = py[q];
-    }
-    if (eb + int64_t(NW) * EB < e1) p2_fetch(eb + int64_t(NW) * EB);  // the next batch
+    for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
     lds_sync<1>();
     for (int k = grp; k < cnt; k += L::G) {
 #pragma unroll
@@ -753,6 +547,29 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       if (k < cnt && q == 0) store_row<D2>(grad_Y + (eb + k) * D2, gy);
     }
   }
+}
+
+// The embedding VJP as a launch of its own, one workgroup of NW waves per
+// center, after a kernel that wrote grad_env (the lmax-3 backward on the
+// matrix cores, whose workgroups each own only 16 channels of a center).
+template <int U, int D2, int NW>
+__global__ __launch_bounds__(kWave * NW) void embedding_vjp_kernel(const int64_t *__restrict__ row_ptr,
+                                                                   const float *__restrict__ grad_env,
+                                                                   const float *__restrict__ w,
+                                                                   const float *__restrict__ Y,
+                                                                   float *__restrict__ grad_w,
+                                                                   float *__restrict__ grad_Y) {
+  constexpr int EB = 8, STAGE = EB * (U + 1 + D2);
+  __shared__ float4 smem[(U * D2 + NW * STAGE + 3) / 4];
+  float *ge_l = reinterpret_cast<float *>(smem);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int64_t n = blockIdx.x;
+  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  if (e1 <= e0) return;
+  const float4 *src = reinterpret_cast<const float4 *>(grad_env + n * U * D2);
+  for (int i = tid; i < U * D2 / 4; i += kWave * NW) reinterpret_cast<float4 *>(ge_l)[i] = src[i];
+  lds_sync<NW>();
+  embedding_vjp<U, D2, NW, EB>(ge_l, ge_l + U * D2 + wave * STAGE, e0, e1, wave, lane, w, Y, grad_w, grad_Y);
 }
 
 // ------------------------------------------------------ tensor product bwd
@@ -829,7 +646,6 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   using B = BwdLds<Core, U, WG, NW>;
   constexpr int D2 = Core::D2, NP = Core::NP, WPT = NW / L::CPL, NT = NW * kWave;
   static_assert(NW % L::CPL == 0, "waves split evenly over the channel halves");
-  static_assert(!WG || Core::LMAX <= 2, "the lmax-3 training backward is tp_backward_g_kernel");
   __shared__ float4 smem[(B::FLOATS + 3) / 4];
   float *lds = reinterpret_cast<float *>(smem);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
@@ -891,66 +707,404 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   }
   lds_sync<NW>();
 
-  // Pass 2: the embedding's VJP through grad_env, in batches of EB edges dealt
-  // round robin to the waves; each wave first stages the batch's w and Y rows
-  // in its own LDS area with one round of coalesced loads:
-  //   grad_w[e,u] = sum_j grad_env[n,u,j] Y[e,j]   lane <-> channel (coalesced stores)
-  //   grad_Y[e,j] = sum_u grad_env[n,u,j] w[e,u]   lane <-> (edge k, channel eighth q):
-  //                 each lane sums U/8 channels, then an xor butterfly over the 8
-  //                 lanes of the edge (operands swapped between partners, so all 8
-  //                 hold the same bits)
-  constexpr int EB = B::EB, WROW = B::WROW;
-  float *wl = lds + B::GE_PART + B::GE_ROW + wave * B::STAGE;
-  float *yl = wl + EB * WROW;
-  const float4 *w4 = reinterpret_cast<const float4 *>(w);
-  float gel[L::CPL][D2];
-#pragma unroll
-  for (int c = 0; c < L::CPL; ++c)
-#pragma unroll
-    for (int j = 0; j < D2; ++j) gel[c][j] = ge_l[(ul + c * kWave) * D2 + j];
-  for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
-    const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
-    lds_sync<1>();  // this wave's previous batch is done with its staged rows
-    for (int i4 = lane; i4 < cnt * (U / 4); i4 += kWave) {
-      const float4 v = w4[eb * (U / 4) + i4];
-      const int r = (4 * i4) / U, c = (4 * i4) % U;
-      float *dst = wl + r * WROW + c;
-      dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
-    }
-    for (int i = lane; i < cnt * D2; i += kWave) yl[i] = Y[eb * D2 + i];
-    lds_sync<1>();
-    for (int k = grp; k < cnt; k += L::G) {
-#pragma unroll
-      for (int c = 0; c < L::CPL; ++c) {
-        float acc = 0.0f;
-#pragma unroll
-        for (int j = 0; j < D2; ++j) acc = __builtin_fmaf(gel[c][j], yl[k * D2 + j], acc);
-        grad_w[(eb + k) * U + ul + c * kWave] = acc;
+  // Pass 2: the embedding's VJP through grad_env
+  embedding_vjp<U, D2, NW, B::EB>(ge_l, lds + B::GE_PART + B::GE_ROW + wave * B::STAGE, e0, e1, wave, lane, w, Y,
+                                  grad_w, grad_Y);
+}
+
+// ------------------------------------- backward at lmax 3 on the matrix cores
+// Per center n and channel u the backward at lmax 3 is two small dense
+// products (d1 = 32 with full parity, 16 without):
+//   grad_x[e][i] = sum_k g[e][k] M[k][i],  M[k][i] = sum_{p=(a(i),b,c(k))} W(p) sum_j C_pijk env[j]
+//   G[k][i]      = sum_{e in seg(n)} g[e][k] x[e][i]
+// (M is the forward's per-center matrix), and the segment sums follow from G:
+//   grad_env[j] = sum_{(k,i)} sum_p W(p) C_pijk G[k][i],
+//   grad_W[p]  += sum_{(k,i)} sum_j C_pijk env[j] G[k][i]   (training only).
+// Both products run on v_mfma_f32_16x16x4f32: for grad_x the 16 edges of a
+// tile are the rows and k the reduction (d1 / 4 steps per 16 columns of i),
+// for G the edges are the reduction (4 per step) and (k, i) the 16 x 16 output
+// tiles.  Lane l = 16 h + c holds, in slot s = (tk * NT + ti) * 4 + r, the cell
+// (k, i) = (16 tk + 4 h + r, 16 ti + c) of M (B operand of grad_x) and of G
+// (accumulator); the generated tables (TPMfmaTab) build M's cells and contract
+// G's cells lane by lane from the sparse coupling table.
+//
+// Work: every wave walks its own sequence of pairs (center n, CPW consecutive
+// channels), CPW = 32 / d1 so that a pair's row of one edge is 128 contiguous
+// bytes (one channel with full parity, two without), pairs dealt round robin
+// over all waves of the persistent grid (one workgroup of 16 waves per compute
+// unit, sharing one copy of the tables).  A pair's edges move in tiles of 16
+// edges; DEPTH tiles (of this pair and the next ones) are in flight in
+// registers at any time, and the tile being multiplied is staged in the wave's
+// own LDS area (x and g, XOR-swizzled 16-byte columns, so that the row reads of
+// the grad_x operand and the column reads of the G operands are conflict-free).
+// There is no barrier between waves: when a pair's first tile comes up, the
+// wave contracts the previous pair's G (spilled to its LDS area) and builds the
+// new pair's M while its next tiles are still arriving and the other waves keep
+// streaming.  Every sum has a fixed order.  The embedding VJP, which needs all
+// channels of grad_env[n], is embedding_vjp_kernel, launched after this kernel.
+constexpr int kMfmaEdges = 16;  // edges per tile
+
+template <bool FULL>
+struct MfmaShape {
+  using Tab = TPMfmaTab<3, FULL>;
+  static constexpr int D1 = Tab::D1, D2 = 16, NT = Tab::NT, S = Tab::S, NP = Tab::NP;
+  static constexpr int ROW = 32;                 // floats of a pair's row of one edge (128 bytes)
+  static constexpr int CPW = ROW / D1;           // channels per pair
+  static constexpr int RF4 = ROW / 4;            // float4 per row
+  static constexpr int LR = kWave / RF4;         // rows per 16-byte load instruction
+  static constexpr int LJ = kMfmaEdges / LR;     // load instructions per tensor and tile
+  static constexpr int TILE = kMfmaEdges * ROW;  // floats of one tensor's tile
+  static constexpr int DEPTH = 3;                // tiles in flight per wave
+  static constexpr int NW = 16, THREADS = kWave * NW;
+  // between tiles a wave's LDS area holds one channel's G spill [S][64] and H or Z
+  static constexpr int GL = S * kWave;
+  static constexpr int HZ = Tab::NZ + 2 > Tab::RZ * kWave ? Tab::NZ + 2 : Tab::RZ * kWave;
+  static constexpr int AREA = (2 * TILE > GL + HZ ? 2 * TILE : GL + HZ + 3) / 4 * 4;
+  static_assert(NP <= 2 * kWave && Tab::WORDS % 4 == 0 && RF4 * LR == kWave && CPW * D1 == ROW, "layout");
+  static constexpr int LDS_FLOATS = Tab::WORDS + NW * AREA;
+  // first H-table row of round r
+  static constexpr int hrow(int r) {
+    int o = 0;
+    for (int q = 0; q < r; ++q) o += Tab::HT[q];
+    return o;
+  }
+};
+
+// LDS position of element (row e, column k) of a tile of 32-float rows: the
+// 16-byte column k / 4 XOR f(e), f(e) = (e & 7) ^ 4 (e & 1), so that 8
+// consecutive rows read at one 16-byte column, two rows 4 s + h, 4 s + h + 1
+// read at 16 consecutive columns, or one row read in 16-byte pieces, hit
+// distinct banks.
+__device__ __forceinline__ int swz32(int e, int k) {
+  const int f = (e & 7) ^ ((e & 1) << 2);
+  return e * 32 + ((((k >> 2) ^ f)) << 2) + (k & 3);
+}
+
+// Buffer accesses of a tile: a descriptor of `bytes` bytes from p (raw, 32-bit
+// dwords), non-temporal 16-byte loads and stores at a byte offset; a load past
+// the range reads zeros and a store past it is dropped.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), short(0), int(bytes), 0x00020000);
+}
+constexpr int kNonTemporal = 2;
+__device__ __forceinline__ f32x4 load_tile_f4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, kNonTemporal));
+}
+__device__ __forceinline__ void store_tile_f4(__amdgpu_buffer_rsrc_t r, uint32_t off, f32x4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, int(off), 0, kNonTemporal);
+}
+
+template <bool FULL, int U, bool WG>
+__global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
+    int64_t N, const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+    const float *__restrict__ path_w, const float *__restrict__ g, float *__restrict__ grad_x,
+    float *__restrict__ grad_env, float *__restrict__ pw_part) {
+  using Sh = MfmaShape<FULL>;
+  using Tab = typename Sh::Tab;
+  constexpr int D1 = Sh::D1, D2 = Sh::D2, NT = Sh::NT, S = Sh::S, NP = Sh::NP, CPW = Sh::CPW;
+  constexpr int RF4 = Sh::RF4, LR = Sh::LR, LJ = Sh::LJ, NW = Sh::NW, DEPTH = Sh::DEPTH, GROUPS = U / CPW;
+  static_assert(U % CPW == 0, "whole pairs");
+  __shared__ float4 smem4[Sh::LDS_FLOATS / 4];
+  float *lds = reinterpret_cast<float *>(smem4);
+  const uint32_t *tab = reinterpret_cast<const uint32_t *>(lds);
+  const uint16_t *tab16 = reinterpret_cast<const uint16_t *>(lds);
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = int(threadIdx.x) % kWave;
+  float *xs = lds + Tab::WORDS + wave * Sh::AREA, *gs = xs + Sh::TILE;
+  float *Gl = xs, *Hz = xs + Sh::GL;  // between tiles
+  {
+    const uint4 *src = reinterpret_cast<const uint4 *>(Tab::words());
+    for (int i = int(threadIdx.x); i < Tab::WORDS / 4; i += Sh::THREADS) reinterpret_cast<uint4 *>(lds)[i] = src[i];
+  }
+  lds_sync<NW>();  // the tables are in LDS (the only barrier of the workgroup)
+  const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x), *g4 = reinterpret_cast<const f32x4 *>(g);
+  f32x4 *gx4 = reinterpret_cast<f32x4 *>(grad_x);
+  const int64_t total = int64_t(gridDim.x) * NW, pairs = N * GROUPS;
+  constexpr uint32_t EDGE_BYTES = U * D1 * 4;  // between consecutive edges in HBM
+  // A lane's offsets within a tile: load lane l moves rows l / RF4 + LR j at
+  // 16-byte column l % RF4; MFMA lane l = 16 h + c.  They are recomputed from
+  // an opaque copy of the lane index where used: held through the loop (they
+  // do not change) they take registers the tiles in flight need.
+  auto opaque_lane = [&]() {
+    int l = lane;
+    __asm__ volatile("" : "+v"(l));
+    return l;
+  };
+  // The tables never change either, so every lookup would be hoisted out of the
+  // pair loop and held; an opaque zero added to the table offsets keeps each
+  // lookup where it is used.
+  auto opaque_zero = []() {
+    int z = 0;
+    __asm__ volatile("" : "+s"(z));
+    return z;
+  };
+
+  // ---- the fetch cursor: the next tile to load (pair fq, edges [feb, feb + 16)).
+  // Everything about it is wave-uniform; saying so keeps the tile addresses a
+  // scalar base plus 32-bit lane offsets.
+  auto uniform = [](int64_t v) {
+    const uint64_t u = uint64_t(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u)), hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+    return int64_t((uint64_t(hi) << 32) | lo);
+  };
+  int64_t fq = int64_t(blockIdx.x) * NW + wave, fn = 0, feb = 0, fe1 = 0;
+  int fu0 = 0;
+  bool fvalid = false, ffirst = false;
+  // pairs of centers without edges have zero sums: written here, no tiles
+  auto seek = [&]() {
+    fvalid = false;
+    while (fq < pairs) {
+      fn = fq / GROUPS;
+      fu0 = int(fq % GROUPS) * CPW;
+      feb = uniform(row_ptr[fn]);
+      fe1 = uniform(row_ptr[fn + 1]);
+      if (fe1 > feb) {
+        fvalid = ffirst = true;
+        return;
       }
+      if (lane < CPW * D2) grad_env[(fn * U + fu0) * D2 + lane] = 0.0f;
+      if constexpr (WG) {
+        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(fn * NP + i / CPW) * U + fu0 + i % CPW] = 0.0f;
+      }
+      fq += total;
     }
-    {
-      constexpr int UQ = U / 8;  // channels per lane
-      const int k = lane / 8, q = lane % 8;
-      const float *wrow = wl + k * WROW + q * UQ;
-      const float *gq = ge_l + q * UQ * D2;
-      float gy[D2];
+  };
+  // the ring of tiles in flight: slot d holds a tile and its identity
+  f32x4 vx[DEPTH][LJ], vg[DEPTH][LJ];
+  int64_t s_n[DEPTH], s_eb[DEPTH], s_e1[DEPTH];
+  int s_u0[DEPTH];
+  bool s_valid[DEPTH], s_first[DEPTH];
+  auto fetch = [&](int d) {
+    s_valid[d] = fvalid;
+    if (!fvalid) return;
+    s_n[d] = fn;
+    s_u0[d] = fu0;
+    s_eb[d] = feb;
+    s_e1[d] = fe1;
+    s_first[d] = ffirst;
+    ffirst = false;
+    // buffer loads from the tile's first row: rows past the segment lie past
+    // the descriptor's range and read as zero
+    const int64_t base = (feb * U + fu0) * (D1 / 4);
+    const uint32_t bytes = uint32_t(fe1 - feb < kMfmaEdges ? fe1 - feb : kMfmaEdges) * EDGE_BYTES;
+    const auto rx = tile_rsrc(x4 + base, bytes), rg = tile_rsrc(g4 + base, bytes);
+    const int ln = opaque_lane();
+    const uint32_t voff = uint32_t(ln / RF4) * EDGE_BYTES + uint32_t(ln % RF4) * 16u;
 #pragma unroll
-      for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
-      if (k < cnt) {
-#pragma unroll 4
-        for (int uu = 0; uu < UQ; ++uu) {
-          const float wv = wrow[uu];
+    for (int j = 0; j < LJ; ++j) {
+      vx[d][j] = load_tile_f4(rx, voff + uint32_t(LR * j) * EDGE_BYTES);
+      vg[d][j] = load_tile_f4(rg, voff + uint32_t(LR * j) * EDGE_BYTES);
+    }
+    feb += kMfmaEdges;
+    if (feb >= fe1) {
+      fq += total;
+      seek();
+    }
+  };
+
+  // the pair whose tiles are being multiplied: its identity, M and G
+  int64_t p_n = 0;
+  int p_u0 = 0;
+  bool have_pair = false;
+  // the pair's path weights and env rows, loaded where they are used (the
+  // prologue and the contraction) rather than held through the tile loop
+  float pw0[CPW], pw1[CPW], pev[CPW];
+  auto load_params = [&]() {
 #pragma unroll
-          for (int j = 0; j < D2; ++j) gy[j] = __builtin_fmaf(gq[uu * D2 + j], wv, gy[j]);
+    for (int cw = 0; cw < CPW; ++cw) {
+      const int u = p_u0 + cw;
+      pw0[cw] = lane < NP ? path_w[lane * U + u] : 0.0f;
+      pw1[cw] = lane + kWave < NP ? path_w[(lane + kWave) * U + u] : 0.0f;
+      pev[cw] = lane < D2 ? env[(p_n * U + u) * D2 + lane] : 0.0f;
+    }
+  };
+  float m[CPW][S];
+  f32x4 Gacc[CPW][NT * NT];
+  // W(p) and env[j] of channel cw of the current pair, from the lanes that hold them
+  auto wp = [&](int cw, int p) {
+    const float a = __shfl(pw0[cw], p & 63), b = __shfl(pw1[cw], p & 63);
+    return p < kWave ? a : b;
+  };
+  auto ej = [&](int cw, int j) { return __shfl(pev[cw], j); };
+
+  // contraction of G for the current pair: spill, H, grad_env, path-weight row
+  auto finish_pair = [&]() {
+    load_params();
+#pragma unroll
+    for (int cw = 0; cw < CPW; ++cw) {
+      const int z0 = opaque_zero();
+      const int u = p_u0 + cw;
+      lds_sync<1>();  // the LDS area (or the previous channel's H) is free
+#pragma unroll
+      for (int t = 0; t < NT * NT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Gl[(t * 4 + r) * kWave + lane] = Gacc[cw][t][r];
+      if (lane == 0) Hz[Tab::NZ] = 0.0f;
+      lds_sync<1>();
+      static_for<0, Tab::RH>([&](auto rc) {
+        constexpr int r = decltype(rc)::value, r0 = Sh::hrow(r);
+        float hv = 0.0f;
+#pragma unroll
+        for (int t = 0; t < Tab::HT[r]; ++t) {
+          const int row = z0 + (r0 + t) * kWave + lane;
+          hv = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_HC + row]), Gl[tab16[2 * Tab::OFF_HI + row]], hv);
+        }
+        Hz[tab16[2 * Tab::OFF_HT + z0 + r * kWave + lane]] = hv;
+        __asm__ volatile("" : : : "memory");
+      });
+      lds_sync<1>();
+      float ge = 0.0f;
+#pragma unroll
+      for (int t = 0; t < Tab::TGE; ++t) {
+        const uint32_t wd = tab[Tab::OFF_GE + z0 + t * kWave + lane];
+        ge = __builtin_fmaf(Hz[wd & 0xffffu], wp(cw, int(wd >> 16)), ge);
+      }
+      ge += __shfl_xor(ge, 1);
+      ge += __shfl_xor(ge, 2);
+      if ((lane & 3) == 0) grad_env[(p_n * U + u) * D2 + lane / 4] = ge;
+      if constexpr (WG) {
+#pragma unroll
+        for (int r = 0; r < Tab::RPW; ++r) {
+          const int p = kWave * r + lane;
+          const uint32_t wd = tab[Tab::OFF_PW + z0 + p];
+          const int off = int(wd & 0xffffu), len = int(wd >> 16);
+          // the shuffle reads env from lanes 0..15, so every lane takes it:
+          // the loop runs to the longest path's length, shorter ones add zeros
+          float a = 0.0f;
+          for (int k = 0; k < Tab::PWMAX; ++k) {
+            const bool in = k < len;
+            const uint32_t zp = tab[Tab::OFF_ZP + z0 + (in ? off + k : 0)];
+            const float e = __shfl(pev[cw], int(zp >> 16));
+            a = __builtin_fmaf(in ? Hz[off + k] : 0.0f, e, a);
+          }
+          if (p < NP) pw_part[(p_n * NP + p) * U + u] = a;
         }
       }
+    }
+  };
+  // the new pair: parameters, Z[q] = W(p) env[j] and M's cells, channel by channel
+  auto start_pair = [&](int64_t n, int u0) {
+    p_n = n;
+    p_u0 = u0;
+    have_pair = true;
+    load_params();
 #pragma unroll
-      for (int off = 1; off < 8; off *= 2)
+    for (int cw = 0; cw < CPW; ++cw) {
+      const int z0 = opaque_zero();
+      lds_sync<1>();  // Hz is free
 #pragma unroll
-        for (int j = 0; j < D2; ++j) gy[j] += __shfl_xor(gy[j], off);
-      if (k < cnt && q == 0) store_row<D2>(grad_Y + (eb + k) * D2, gy);
+      for (int r = 0; r < Tab::RZ; ++r) {
+        const uint32_t pj = tab[Tab::OFF_ZP + z0 + kWave * r + lane];
+        Hz[kWave * r + lane] = wp(cw, int(pj & 0xffffu)) * ej(cw, int(pj >> 16));
+      }
+      lds_sync<1>();
+#pragma unroll
+      for (int sl = 0; sl < S; ++sl) {
+        float a = 0.0f;
+#pragma unroll
+        for (int t = 0; t < Tab::MT; ++t) {
+          const int row = z0 + (t * S + sl) * kWave + lane;
+          a = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_MC + row]), Hz[tab16[2 * Tab::OFF_MI + row]], a);
+        }
+        m[cw][sl] = a;
+      }
+#pragma unroll
+      for (int t = 0; t < NT * NT; ++t) Gacc[cw][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+    lds_sync<1>();  // Hz is read before the tile overwrites it
+  };
+  // one tile, from ring slot d: grad_x rows out, G accumulated
+  auto tile = [&](int d) {
+    if (s_first[d]) {
+      if (have_pair) finish_pair();
+      start_pair(s_n[d], s_u0[d]);
+    }
+    const int64_t teb = s_eb[d], te1 = s_e1[d];
+    int ln = opaque_lane();
+    {
+      const int le = ln / RF4, lc = ln % RF4;
+#pragma unroll
+      for (int j = 0; j < LJ; ++j) {
+        *reinterpret_cast<f32x4 *>(xs + swz32(le + LR * j, 4 * lc)) = vx[d][j];
+        *reinterpret_cast<f32x4 *>(gs + swz32(le + LR * j, 4 * lc)) = vg[d][j];
+      }
+    }
+    fetch(d);  // the slot takes the tile DEPTH ahead
+    lds_sync<1>();
+    const int h = ln / 16, c = ln % 16;
+#pragma unroll
+    for (int cw = 0; cw < CPW; ++cw) {
+      // grad_x[e][i] = sum_k g[e][k] M[k][i]: A = the g rows of the 16 edges
+      f32x4 gA[NT];
+#pragma unroll
+      for (int tk = 0; tk < NT; ++tk)
+        gA[tk] = *reinterpret_cast<const f32x4 *>(gs + swz32(c, D1 * cw + 16 * tk + 4 * h));
+      f32x4 D[NT];
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) {
+        D[ti] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            D[ti] = __builtin_amdgcn_mfma_f32_16x16x4f32(gA[tk][r], m[cw][(tk * NT + ti) * 4 + r], D[ti], 0, 0, 0);
+      }
+      // G[k][i] += sum_e g[e][k] x[e][i], four edges (4 st + h) per step
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        float gG[NT], xG[NT];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const int o = swz32(4 * st + h, D1 * cw + 16 * t + c);
+          gG[t] = gs[o];
+          xG[t] = xs[o];
+        }
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk)
+#pragma unroll
+          for (int ti = 0; ti < NT; ++ti)
+            Gacc[cw][tk * NT + ti] =
+                __builtin_amdgcn_mfma_f32_16x16x4f32(gG[tk], xG[ti], Gacc[cw][tk * NT + ti], 0, 0, 0);
+      }
+      // this channel's x columns are no longer needed: its grad_x rows go there
+      lds_sync<1>();
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) xs[swz32(4 * h + r, D1 * cw + 16 * ti + c)] = D[ti][r];
+    }
+    lds_sync<1>();
+    {
+      // rows past the segment lie past the descriptor's range: not written
+      const uint32_t bytes = uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES;
+      const auto ro = tile_rsrc(gx4 + (teb * U + p_u0) * (D1 / 4), bytes);
+      ln = opaque_lane();
+      const int se = ln / RF4, sc = ln % RF4;
+      const uint32_t voff = uint32_t(se) * EDGE_BYTES + uint32_t(sc) * 16u;
+#pragma unroll
+      for (int j = 0; j < LJ; ++j)
+        store_tile_f4(ro, voff + uint32_t(LR * j) * EDGE_BYTES,
+                      *reinterpret_cast<const f32x4 *>(xs + swz32(se + LR * j, 4 * sc)));
+    }
+    lds_sync<1>();  // the LDS area is free again
+  };
+
+  seek();
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) fetch(d);
+  bool more = true;
+  while (more) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      if (more) {
+        if (s_valid[d])
+          tile(d);
+        else
+          more = false;
+      }
     }
   }
+  if (have_pair) finish_pair();
 }
 
 // ------------------------------------------------------ spherical harmonics
@@ -1162,19 +1316,48 @@ void launch_fwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, con
                        out);
 }
 
+// Persistent grid of the matrix-core backward: the workgroups resident on the
+// device at once (compute units x workgroups per unit), at most one wave per
+// pair of work.  Looked up once per device and kernel.
+template <bool FULL, int U, bool WG>
+unsigned mfma_grid(int64_t N) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static int resident[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
+  int res;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (!resident[dev]) {
+      int cus = 0, per = 0;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, tp_mfma_bwd_kernel<FULL, U, WG>,
+                                                       MfmaShape<FULL>::THREADS, 0) != hipSuccess ||
+          per < 1)
+        per = 1;
+      resident[dev] = cus * per;
+    }
+    res = resident[dev];
+  }
+  const int64_t pairs = N * (U / MfmaShape<FULL>::CPW);
+  const int64_t blocks = (pairs + MfmaShape<FULL>::NW - 1) / MfmaShape<FULL>::NW;
+  return unsigned(blocks < res ? blocks : res);
+}
+
 template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
                 float *pw_part) {
-  if constexpr (WG && Core::LMAX >= 3) {
-    // training backward at lmax 3: grad_x = M^T g, then the segment sums from G
-    hipLaunchKernelGGL((tp_matrix_kernel<Core, U, TPMBwdX<Core::LMAX, Core::FULL>>), grid, dim3(kMFwdThreads<Core>), 0,
-                       s, rp, g, env, pw, gx);
-    hipLaunchKernelGGL((tp_backward_g_kernel<Core, U, 0>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g, w,
-                       Y, genv, gw, gy, pw_part);
-    if constexpr (U > kWave)
-      hipLaunchKernelGGL((tp_backward_g_kernel<Core, U, 1>), grid, dim3(kMFwdThreads<Core>), 0, s, rp, x, env, pw, g,
-                         w, Y, genv, gw, gy, pw_part);
+  if constexpr (Core::LMAX >= 3 && WG) {
+    // training backward at lmax 3: grad_x, grad_env and the path-weight rows on
+    // the matrix cores (one read of x and g), then the embedding VJP from the
+    // complete grad_env.  The inference backward stays on the direct kernel,
+    // which is faster there (10.6 against 12.6 ms on 20,000 centers, U = 128).
+    const int64_t N = grid.x;
+    hipLaunchKernelGGL((tp_mfma_bwd_kernel<Core::FULL, U, WG>), dim3(mfma_grid<Core::FULL, U, WG>(N)),
+                       dim3(MfmaShape<Core::FULL>::THREADS), 0, s, N, rp, x, env, pw, g, gx, genv, pw_part);
+    hipLaunchKernelGGL((embedding_vjp_kernel<U, Core::D2, 4>), grid, dim3(kWave * 4), 0, s, rp, genv, w, Y, gw, gy);
   } else {
     hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x,
                        env, pw, g, w, Y, gx, genv, gw, gy, pw_part);
@@ -1270,6 +1453,14 @@ unsigned env_blocks(int U, int64_t N) {
 
 extern "C" {
 
+// Failure injection for tests: ALLEGRO_SIMULATE_ALLOC_FAILURE = "plan", "table"
+// or "status" makes that allocation of plan creation fail as if memory were
+// exhausted (the status word's hipMalloc is then not called).
+static bool simulated_alloc_failure(const char *what) {
+  const char *v = std::getenv("ALLEGRO_SIMULATE_ALLOC_FAILURE");
+  return v && std::strcmp(v, what) == 0;
+}
+
 int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags) {
   if (!plan) return fail(ALLEGRO_E_INVALID, "plan output pointer is NULL");
   *plan = nullptr;
@@ -1278,20 +1469,31 @@ int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags) {
     return fail(ALLEGRO_E_UNSUPPORTED, "U=%d not supported (16, 32, 64 or 128)", U);
   if (flags & ~(ALLEGRO_FULL_PARITY | ALLEGRO_DETERMINISTIC | ALLEGRO_VALIDATE))
     return fail(ALLEGRO_E_INVALID, "unknown flags 0x%x", flags);
-  allegro_tp_plan *p = new (std::nothrow) allegro_tp_plan;
+  allegro_tp_plan *p = simulated_alloc_failure("plan") ? nullptr : new (std::nothrow) allegro_tp_plan;
   if (!p) return fail(ALLEGRO_E_NOMEM, "plan allocation failed");
   p->lmax = lmax;
   p->U = U;
   p->flags = flags;
   try {
+    if (simulated_alloc_failure("table")) throw std::bad_alloc();
     p->table = allegro::build_table(lmax, (flags & ALLEGRO_FULL_PARITY) != 0);
+  } catch (const std::bad_alloc &) {
+    delete p;
+    return fail(ALLEGRO_E_NOMEM, "coupling table allocation failed");
   } catch (const std::exception &ex) {
     delete p;
     return fail(ALLEGRO_E_INVALID, "coupling table build failed: %s", ex.what());
   }
-  if ((flags & ALLEGRO_VALIDATE) && hipMalloc(&p->status, sizeof(int)) != hipSuccess) {
-    delete p;
-    return fail(ALLEGRO_E_NOMEM, "device status word allocation failed: %s", hipGetErrorString(hipGetLastError()));
+  if (flags & ALLEGRO_VALIDATE) {
+    if (simulated_alloc_failure("status")) {
+      delete p;
+      return fail(ALLEGRO_E_NOMEM, "device status word allocation failed (simulated)");
+    }
+    if (hipMalloc(&p->status, sizeof(int)) != hipSuccess) {
+      p->status = nullptr;
+      delete p;
+      return fail(ALLEGRO_E_NOMEM, "device status word allocation failed: %s", hipGetErrorString(hipGetLastError()));
+    }
   }
   *plan = p;
   return ALLEGRO_OK;

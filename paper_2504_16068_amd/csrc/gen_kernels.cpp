@@ -19,7 +19,10 @@
 //
 // Usage: gen_kernels <output.inc>
 #include <algorithm>
+#include <cstdint>
 #include <cstdio>
+#include <cstring>
+#include <stdexcept>
 #include <map>
 #include <set>
 #include <string>
@@ -217,15 +220,11 @@ void emit_core(FILE *f, const allegro::TPTable &t) {
 // NW waves (ROWS consecutive rows each); wave w builds its rows once per
 // center and applies them to every edge.  Emitted for lmax 3, where it takes
 // about half the arithmetic of the direct contraction per edge.
-//
-// With transpose the rows are the x components i and the columns the output
-// components k: grad_x[i] = sum_k M[k][i] g[k], the VJP of the forward with
-// respect to x.
-void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name, bool transpose) {
+void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name) {
   const int d1 = t.d1, rows = d1 / nw;
-  // (row, column) -> list of (path, j, C); row = k and column = i, or the reverse
+  // (row k, column i) -> list of (path, j, C)
   std::map<std::pair<int, int>, std::vector<allegro::CGEntry>> cells;
-  for (const auto &e : t.entries) cells[transpose ? std::make_pair(e.i, e.k) : std::make_pair(e.k, e.i)].push_back(e);
+  for (const auto &e : t.entries) cells[{e.k, e.i}].push_back(e);
   int maxm = 0;
   std::vector<std::vector<std::pair<int, int>>> wave_cells(nw);
   for (int w = 0; w < nw; ++w) {
@@ -290,75 +289,173 @@ void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name, b
   std::fprintf(f, "      default: break;\n    }\n  }\n};\n\n");
 }
 
-// The segment sums of the backward from the per-center matrix of products
-// G[k][i] = sum over the center's edges of x[i] g[k] (rows k split over the
-// waves as in TPMFwd, only the (k, i) cells that carry coupling entries):
-//   grad_env[j] = sum_{(k,i)} sum_{p: (p,i,j,k)} W(p) C_pijk G[k][i]
-//   grad_W[p]   = sum_{(k,i)} sum_j C_pijk env[j] G[k][i]
-// accumulate() adds one edge to the wave's cells; finish_ge() and finish_gw()
-// add the wave's part of the two sums into ge and gw (which the caller zeroes).
-void emit_genv(FILE *f, const allegro::TPTable &t, int nw) {
-  const int d1 = t.d1, rows = d1 / nw;
-  std::map<std::pair<int, int>, std::vector<allegro::CGEntry>> cells;  // (k, i)
-  for (const auto &e : t.entries) cells[{e.k, e.i}].push_back(e);
-  int maxm = 0;
-  std::vector<std::vector<std::pair<int, int>>> wave_cells(nw);
-  for (int w = 0; w < nw; ++w) {
-    for (const auto &kv : cells)
-      if (kv.first.first / rows == w) wave_cells[w].push_back(kv.first);
-    maxm = std::max(maxm, int(wave_cells[w].size()));
+// Lane tables of the matrix-core backward at lmax 3 (tp_mfma_bwd_kernel).
+//
+// Per (center, channel) the backward needs two small dense products:
+//   grad_x[e][i] = sum_k g[e][k] M[k][i]      (M the per-center matrix of the forward)
+//   G[k][i]      = sum_e g[e][k] x[e][i]      (per-center products)
+// which run on v_mfma_f32_16x16x4f32.  In its operand and result layout lane
+// l = 16 h + c of a wave holds, for slot s = (tk * NT + ti) * 4 + r, the cell
+//   (k, i) = (16 tk + 4 h + r, 16 ti + c)
+// of M (as the B operand of grad_x, K = k) and of G (as the accumulator), so one
+// assignment of cells to (lane, slot) serves both.  The tables let every lane
+// form its own cells of M and contract its cells of G without any lane-uniform
+// code:
+//   Z[q] = W(p) env[j] for the q-th distinct (p, j) of the coupling table
+//          (rounds of 64 lanes; word p | j << 16 per lane);
+//   M[s] = sum_t MC[t][s][lane] Z[MI[t][s][lane]]   (at most MT terms per cell,
+//          padded with zero coefficients);
+//   H[q] = sum over the cells (k, i) of path p, env component j of C_pijk G[k][i]
+//          (H rounds: lane -> target q, HT[round] terms of (coefficient, index
+//          of the cell in the wave's G spill [slot][64]));
+//   grad_env[j] = sum_q W(p(q)) H[q] over the q with j(q) = j: lane 4 j + quarter
+//          sums every fourth such q (words q | p << 16, padded with q = NZ,
+//          where H[NZ] = 0), then the four quarters are added by lane shuffles;
+//   grad_W[p]   = sum over the q of path p (contiguous from off, len of them) of
+//          env[j(q)] H[q] (word off | len << 16).
+// All tables are packed into one array of 32-bit words (floats as their bit
+// patterns, 16-bit indices two per word), copied to LDS once per workgroup.
+void emit_mfma_tables(FILE *f, const allegro::TPTable &t) {
+  const int d1 = t.d1, np = int(t.paths.size()), nt = d1 / 16, S = nt * nt * 4;
+  if (d1 % 16 != 0 || t.d2 != 16) throw std::runtime_error("matrix-core tables need d1 % 16 == 0 and d2 == 16");
+  // distinct (p, j), sorted
+  std::map<std::pair<int, int>, int> zq;
+  for (const auto &e : t.entries) zq[{e.path, e.j}] = 0;
+  std::vector<std::pair<int, int>> zlist;
+  for (auto &kv : zq) {
+    kv.second = int(zlist.size());
+    zlist.push_back(kv.first);
   }
-  std::fprintf(f, "template <> struct TPGEnv<%d, %s> {\n", t.lmax, t.full_parity ? "true" : "false");
-  std::fprintf(f, "  static constexpr int NW = %d, ROWS = %d, MAXM = %d;\n", nw, rows, maxm);
-  std::fprintf(f, "  static __device__ __forceinline__ void accumulate(int w, const float (&x)[%d], const float (&g)[ROWS], "
-                  "float (&G)[MAXM]) {\n    switch (w) {\n", d1);
-  for (int w = 0; w < nw; ++w) {
-    std::fprintf(f, "      case %d:\n", w);
-    for (int q = 0; q < int(wave_cells[w].size()); ++q)
-      std::fprintf(f, "        G[%d] = __builtin_fmaf(x[%d], g[%d], G[%d]);\n", q, wave_cells[w][q].second,
-                   wave_cells[w][q].first - w * rows, q);
-    std::fprintf(f, "        break;\n");
+  const int nz = int(zlist.size()), rz = (nz + 63) / 64;
+  auto cell_of = [&](int lane, int slot) {
+    const int h = lane / 16, c = lane % 16, r = slot % 4, tk = (slot / 4) / nt, ti = (slot / 4) % nt;
+    return std::make_pair(16 * tk + 4 * h + r, 16 * ti + c);  // (k, i)
+  };
+  auto gidx_of = [&](int k, int i) {  // position of cell (k, i) in the [slot][64] spill
+    const int tk = k / 16, h = (k % 16) / 4, r = k % 4, ti = i / 16, c = i % 16;
+    return ((tk * nt + ti) * 4 + r) * 64 + 16 * h + c;
+  };
+  // M terms per cell
+  std::map<std::pair<int, int>, std::vector<std::pair<double, int>>> mterms;
+  for (const auto &e : t.entries) mterms[{e.k, e.i}].push_back({e.value, zq[{e.path, e.j}]});
+  int mt = 0;
+  for (const auto &kv : mterms) mt = std::max(mt, int(kv.second.size()));
+  // H terms per (p, j); rounds by descending term count
+  std::vector<std::vector<std::pair<double, int>>> hterms(nz);
+  for (const auto &e : t.entries) hterms[zq[{e.path, e.j}]].push_back({e.value, gidx_of(e.k, e.i)});
+  std::vector<int> order(nz);
+  for (int q = 0; q < nz; ++q) order[q] = q;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return hterms[a].size() > hterms[b].size(); });
+  const int rh = (nz + 63) / 64;
+  std::vector<int> ht(rh, 0);
+  for (int k = 0; k < nz; ++k) ht[k / 64] = std::max(ht[k / 64], int(hterms[order[k]].size()));
+  int th = 0;
+  for (int v : ht) th += v;
+  // grad_env lists: lane 4 j + quarter
+  std::vector<std::vector<int>> ge_lane(64);
+  for (int j = 0; j < 16; ++j) {
+    std::vector<int> qs;
+    for (int q = 0; q < nz; ++q)
+      if (zlist[q].second == j) qs.push_back(q);
+    for (size_t n = 0; n < qs.size(); ++n) ge_lane[4 * j + int(n % 4)].push_back(qs[n]);
   }
-  std::fprintf(f, "      default: break;\n    }\n  }\n");
-  // finish_ge: ge[j] += sum over the wave's cells of W(p) C_pijk G[q]
-  std::fprintf(f, "  template <class WT>\n  static __device__ __forceinline__ void finish_ge(int w, const WT &W, "
-                  "const float (&G)[MAXM], float (&ge)[%d]) {\n    switch (w) {\n", t.d2);
-  for (int w = 0; w < nw; ++w) {
-    std::fprintf(f, "      case %d:\n", w);
-    for (int q = 0; q < int(wave_cells[w].size()); ++q) {
-      std::map<int, std::vector<allegro::CGEntry>> by_path;
-      for (const auto &e : cells[wave_cells[w][q]]) by_path[e.path].push_back(e);
-      for (const auto &pv : by_path) {
-        std::fprintf(f, "        { const float t = W(%d) * G[%d];", pv.first, q);
-        for (const auto &e : pv.second)
-          std::fprintf(f, " ge[%d] = __builtin_fmaf(%s, t, ge[%d]);", e.j, lit(e.value).c_str(), e.j);
-        std::fprintf(f, " }\n");
+  int tge = 0;
+  for (const auto &v : ge_lane) tge = std::max(tge, int(v.size()));
+  const int rpw = (np + 63) / 64;
+  // pack
+  std::vector<uint32_t> words;
+  auto fbits = [](double v) {
+    const float x = float(v);
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    return u;
+  };
+  auto push16 = [&](const std::vector<int> &v) {  // 64 indices -> 32 words
+    for (int l = 0; l < 64; l += 2) words.push_back(uint32_t(v[l]) | (uint32_t(v[l + 1]) << 16));
+  };
+  const int off_mc = int(words.size());
+  for (int tt = 0; tt < mt; ++tt)
+    for (int sl = 0; sl < S; ++sl)
+      for (int l = 0; l < 64; ++l) {
+        const auto &v = mterms[cell_of(l, sl)];
+        words.push_back(fbits(tt < int(v.size()) ? v[tt].first : 0.0));
       }
-    }
-    std::fprintf(f, "        break;\n");
-  }
-  std::fprintf(f, "      default: break;\n    }\n  }\n");
-  // finish_gw: gw[p] += sum over the wave's cells of (sum_j C_pijk env[j]) G[q]
-  std::fprintf(f, "  static __device__ __forceinline__ void finish_gw(int w, const float *__restrict__ env, "
-                  "const float (&G)[MAXM], float (&gw)[%d]) {\n    switch (w) {\n", int(t.paths.size()));
-  for (int w = 0; w < nw; ++w) {
-    std::fprintf(f, "      case %d:\n", w);
-    for (int q = 0; q < int(wave_cells[w].size()); ++q) {
-      std::map<int, std::vector<allegro::CGEntry>> by_path;
-      for (const auto &e : cells[wave_cells[w][q]]) by_path[e.path].push_back(e);
-      for (const auto &pv : by_path) {
-        std::fprintf(f, "        { float s;");
-        bool first = true;
-        for (const auto &e : pv.second) {
-          std::fprintf(f, " %s", accumulate("s", first, e.value, "env[" + std::to_string(e.j) + "]").c_str());
-          first = false;
-        }
-        std::fprintf(f, " gw[%d] = __builtin_fmaf(s, G[%d], gw[%d]); }\n", pv.first, q, pv.first);
+  const int off_zp = int(words.size());
+  for (int q = 0; q < rz * 64; ++q)
+    words.push_back(q < nz ? uint32_t(zlist[q].first) | (uint32_t(zlist[q].second) << 16) : 0u);
+  const int off_hc = int(words.size());
+  for (int r = 0; r < rh; ++r)
+    for (int tt = 0; tt < ht[r]; ++tt)
+      for (int l = 0; l < 64; ++l) {
+        const int k = 64 * r + l;
+        const bool ok = k < nz && tt < int(hterms[order[k]].size());
+        words.push_back(fbits(ok ? hterms[order[k]][tt].first : 0.0));
       }
+  const int off_ge = int(words.size());
+  for (int tt = 0; tt < tge; ++tt)
+    for (int l = 0; l < 64; ++l) {
+      const int q = tt < int(ge_lane[l].size()) ? ge_lane[l][tt] : nz;
+      const int pth = q < nz ? zlist[q].first : 0;
+      words.push_back(uint32_t(q) | (uint32_t(pth) << 16));
     }
-    std::fprintf(f, "        break;\n");
+  const int off_pw = int(words.size());
+  int pwmax = 0;
+  for (int p = 0; p < rpw * 64; ++p) {
+    int off = 0, len = 0;
+    for (int q = 0; q < nz; ++q)
+      if (zlist[q].first == p) {
+        if (!len) off = q;
+        if (q != off + len) throw std::runtime_error("the (p, j) list of a path is not contiguous");
+        ++len;
+      }
+    pwmax = std::max(pwmax, len);
+    words.push_back(uint32_t(off) | (uint32_t(len) << 16));
   }
-  std::fprintf(f, "      default: break;\n    }\n  }\n};\n\n");
+  const int off_mi = int(words.size());
+  for (int tt = 0; tt < mt; ++tt)
+    for (int sl = 0; sl < S; ++sl) {
+      std::vector<int> v(64);
+      for (int l = 0; l < 64; ++l) {
+        const auto &m = mterms[cell_of(l, sl)];
+        v[l] = tt < int(m.size()) ? m[tt].second : 0;
+      }
+      push16(v);
+    }
+  const int off_hi = int(words.size());
+  for (int r = 0; r < rh; ++r)
+    for (int tt = 0; tt < ht[r]; ++tt) {
+      std::vector<int> v(64);
+      for (int l = 0; l < 64; ++l) {
+        const int k = 64 * r + l;
+        v[l] = (k < nz && tt < int(hterms[order[k]].size())) ? hterms[order[k]][tt].second : 0;
+      }
+      push16(v);
+    }
+  const int off_ht = int(words.size());
+  for (int r = 0; r < rh; ++r) {
+    std::vector<int> v(64);
+    for (int l = 0; l < 64; ++l) v[l] = 64 * r + l < nz ? order[64 * r + l] : nz + 1;
+    push16(v);
+  }
+  while (words.size() % 4) words.push_back(0u);
+  const char *full = t.full_parity ? "true" : "false";
+  std::fprintf(f, "template <> struct TPMfmaTab<%d, %s> {\n", t.lmax, full);
+  std::fprintf(f, "  static constexpr int D1 = %d, NT = %d, S = %d, NP = %d, NZ = %d, RZ = %d, MT = %d, RH = %d, TH = %d, "
+                  "TGE = %d, RPW = %d, PWMAX = %d;\n", d1, nt, S, np, nz, rz, mt, rh, th, tge, rpw, pwmax);
+  std::fprintf(f, "  static constexpr int HT[%d] = {", rh);
+  for (int r = 0; r < rh; ++r) std::fprintf(f, "%s%d", r ? ", " : "", ht[r]);
+  std::fprintf(f, "};\n");
+  std::fprintf(f, "  static constexpr int OFF_MC = %d, OFF_ZP = %d, OFF_HC = %d, OFF_GE = %d, OFF_PW = %d, OFF_MI = %d, "
+                  "OFF_HI = %d, OFF_HT = %d, WORDS = %d;\n", off_mc, off_zp, off_hc, off_ge, off_pw, off_mi, off_hi,
+               off_ht, int(words.size()));
+  std::fprintf(f, "  static __device__ const uint32_t *words();\n};\n");
+  std::fprintf(f, "static __device__ __attribute__((aligned(16))) const uint32_t kMfmaTab%d%s[%d] = {", t.lmax,
+               t.full_parity ? "F" : "N", int(words.size()));
+  for (size_t q = 0; q < words.size(); ++q)
+    std::fprintf(f, "%s0x%08x", q == 0 ? "\n  " : (q % 8 ? ", " : ",\n  "), words[q]);
+  std::fprintf(f, "};\n");
+  std::fprintf(f, "__device__ inline const uint32_t *TPMfmaTab<%d, %s>::words() { return kMfmaTab%d%s; }\n\n", t.lmax,
+               full, t.lmax, t.full_parity ? "F" : "N");
 }
 
 }  // namespace
@@ -378,16 +475,15 @@ int main(int argc, char **argv) {
                "#pragma once\n\n"
                "template <int LMAX, bool FULL> struct TPCore;\n"
                "template <int LMAX, bool FULL> struct TPMFwd;\n"
-               "template <int LMAX, bool FULL> struct TPMBwdX;\n"
-               "template <int LMAX, bool FULL> struct TPGEnv;\n\n");
+
+               "template <int LMAX, bool FULL> struct TPMfmaTab;\n\n");
   try {
     for (int lmax = 1; lmax <= 3; ++lmax)
       for (int full = 0; full <= 1; ++full) emit_core(f, allegro::build_table(lmax, full != 0));
     for (int full = 0; full <= 1; ++full) {
       const allegro::TPTable t3 = allegro::build_table(3, full != 0);
-      emit_matrix(f, t3, 8, "TPMFwd", false);
-      emit_matrix(f, t3, 8, "TPMBwdX", true);
-      emit_genv(f, t3, 8);
+      emit_matrix(f, t3, 8, "TPMFwd");
+      emit_mfma_tables(f, t3);
     }
   } catch (const std::exception &ex) {
     std::fprintf(stderr, "gen_kernels: %s\n", ex.what());

@@ -150,6 +150,27 @@ def test_plan_create_rejects_bad_arguments():
     assert lib.allegro_tp_plan_destroy(None) == binding.ALLEGRO_OK
 
 
+@pytest.mark.parametrize("where,flags", [("plan", 1), ("table", 1), ("status", 1 | 4)])
+def test_plan_create_reports_allocation_failure(monkeypatch, where, flags):
+    """A simulated out-of-memory in each allocation of plan creation returns
+    ALLEGRO_E_NOMEM, leaves *plan NULL and names the allocation; the status
+    word (ALLEGRO_VALIDATE) fails before any HIP call."""
+    lib = binding.library()
+    h = ctypes.c_void_p(0x1234)
+    monkeypatch.setenv("ALLEGRO_SIMULATE_ALLOC_FAILURE", where)
+    rc, msg = _err(lib.allegro_tp_plan_create, ctypes.byref(h), 3, 128, flags)
+    assert rc == binding.ALLEGRO_E_NOMEM and not h.value
+    assert {"plan": "plan allocation", "table": "table allocation", "status": "status word"}[where] in msg
+    with pytest.raises(binding.AllegroError) as ex:
+        binding.allegro_tp_plan_create(3, 128, flags)
+    assert ex.value.code == binding.ALLEGRO_E_NOMEM
+    monkeypatch.delenv("ALLEGRO_SIMULATE_ALLOC_FAILURE")
+    if where != "status":  # without the hook the same call succeeds (no GPU needed)
+        rc, _ = _err(lib.allegro_tp_plan_create, ctypes.byref(h), 3, 128, flags)
+        assert rc == binding.ALLEGRO_OK and h.value
+        assert lib.allegro_tp_plan_destroy(h) == binding.ALLEGRO_OK
+
+
 def test_entry_points_reject_bad_arguments_before_any_launch():
     lib = binding.library()
     plan = binding.allegro_tp_plan_create(2, 64, binding.ALLEGRO_FULL_PARITY)
