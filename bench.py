@@ -12,15 +12,21 @@ N(0, 1/sqrt(30)).  Synthetic data: no dataset of the paper is used.
 
 Prints ONE JSON line.  The roofline object describes the dominant kernel
 (tp_backward): algorithmic bytes per launch over its mean duration, measured
-with HIP events on the stream the library launches on.  cpu_baseline times
-the fp64 oracle on a prefix of whole center segments, one thread per host core.
+with HIP events on the stream the library launches on, against the 8 TB/s
+HBM peak and against the rate of a plain streaming kernel of the same access
+pattern timed in the same run (stream_probes).  Extra keys:
+  high_order      the same step at Table I's large-model shape (lmax 3, 128
+                  channels), with its own roofline object;
+  allegro_layer   one whole Allegro layer (forward, and backward with every
+                  weight gradient) at the medium model shape of Table I;
+  cpu_baseline    the fp64 oracle on bounded samples of the small, headline and
+                  high-order workloads, timed before the GPU is touched.
 
-The allegro_layer object times one whole Allegro layer (forward, and backward
-with every weight gradient) at the medium model shape of Table I, outside the
-step.
-
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-layer]
-       python bench.py --pmc-summary FETCH_CSV WRITE_CSV   (after two rocprofv3 --pmc runs)
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--no-cpu-baseline] [--no-layer] [--no-high-order]
+       python bench.py --layer-only
+       python bench.py --pmc-summary FETCH_CSV WRITE_CSV --pmc-kernel NAME
+                       (after two rocprofv3 --pmc runs; see pmc_summary)
 """
 
 from __future__ import annotations
@@ -28,8 +34,8 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
-import re
 import os
+import re
 import sys
 import time
 
@@ -43,11 +49,29 @@ import workloads  # noqa: E402
 
 METRIC = "Allegro TP fwd+bwd edges/sec at lmax=2, 64 ch; % of HBM (or MFMA) roofline"
 HBM_PEAK_GBPS = 8000.0
-PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "tp_backward_headline_traffic.json")
+HOST_SHARE = 16  # host cores that go with one GPU on the MI355X hosts
+PROFILES = os.path.join(ROOT, "profiles")
+# kernels with committed rocprofv3 traffic records (profiles/<kernel>_<workload>_traffic.json):
+# the kernel-name pattern of each
+TRAFFIC_KERNELS = {
+    "tp_backward": r"tp_backward_kernel<TPCore<\d+,\s*(true|false)>,\s*\d+,\s*false(,\s*\d+)?>",
+    "tp_forward": r"tp_(forward|matrix)_kernel<TPCore<\d+,\s*(true|false)>,\s*\d+(,\s*\d+)?(,\s*TPMFwd<[^>]*>\s*)?>",
+    "tp_mfma_bwd": r"tp_mfma_bwd_kernel<(true|false),\s*\d+,\s*true>",
+}
+
+
+def traffic_record_path(kernel: str, workload: str) -> str:
+    return os.path.join(PROFILES, f"{kernel}_{workload}_traffic.json")
+# the sources the kernels are built from, with their build flags
+DIGEST_SOURCES = ("paper_2504_16068_amd/csrc/allegro_tp.hip", "paper_2504_16068_amd/csrc/allegro_layer.hip",
+                  "paper_2504_16068_amd/csrc/device_common.hpp", "paper_2504_16068_amd/csrc/plan.hpp",
+                  "paper_2504_16068_amd/csrc/gen_kernels.cpp", "paper_2504_16068_amd/csrc/cg_builder.cpp",
+                  "paper_2504_16068_amd/csrc/cg_builder.hpp", "paper_2504_16068_amd/build.py",
+                  "include/allegro_tp.h", "include/allegro_layer.h")
 
 
 def algorithmic_bytes(cfg, n_atoms: int, n_edges: int):
-    """Bytes each kernel must move at least once (fp32 data, int64 row_ptr).
+    """Bytes each call must move at least once (fp32 data, int64 row_ptr).
 
     env_embed:   read w [E,U] and Y [E,d2]; write env [N,U,d2]
     tp_forward:  read x [E,U,d1] and env; write out [E,U,d1]
@@ -64,36 +88,45 @@ def algorithmic_bytes(cfg, n_atoms: int, n_edges: int):
     return {"env_embed": env_b, "tp_forward": fwd_b, "tp_backward": bwd_b}
 
 
+def mfma_bwd_bytes(cfg, n_atoms: int, n_edges: int):
+    """Algorithmic bytes of the lmax-3 training backward's first kernel (tp_mfma_bwd_kernel):
+    read x, g [E,U,d1] and env; write grad_x [E,U,d1], grad_env [N,U,d2] and the
+    per-center path-weight rows [N,P,U]."""
+    d1, d2, n_paths = workloads.dims(cfg.lmax, cfg.full_parity)
+    u = cfg.U
+    return (4 * (3 * n_edges * u * d1 + 2 * n_atoms * u * d2 + n_atoms * n_paths * u) + (n_atoms + 1) * 8
+            + n_paths * u * 4)
+
+
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    # every source the tensor-product kernels are compiled from
-    for rel in ("paper_2504_16068_amd/csrc/allegro_tp.hip", "paper_2504_16068_amd/csrc/device_common.hpp",
-                "paper_2504_16068_amd/csrc/gen_kernels.cpp", "paper_2504_16068_amd/csrc/cg_builder.cpp",
-                "paper_2504_16068_amd/csrc/cg_builder.hpp"):
+    for rel in DIGEST_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per tp_backward launch from the committed rocprofv3 counters, if they
-    were taken on the current kernel sources and this workload; else None."""
-    if not os.path.exists(PROFILE_TRAFFIC):
+def measured_traffic(key: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 record, if it was taken on the
+    current kernel sources and this workload; else None."""
+    path = traffic_record_path(key, workload)
+    if not os.path.exists(path):
         return None
-    with open(PROFILE_TRAFFIC) as f:
+    with open(path) as f:
         rec = json.load(f)
     if rec.get("kernel_source_digest") != kernel_source_digest() or rec.get("workload") != workload:
         return None
     return rec.get("traffic_bytes_per_launch")
 
 
-def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
-    """Calibrated HBM traffic of tp_backward from two rocprofv3 --pmc runs of this script.
+def pmc_summary(fetch_csv: str, write_csv: str, workload: str, key: str):
+    """Calibrated HBM traffic of one kernel from two rocprofv3 --pmc runs of this script.
 
     FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same
-    counter reads for the 4 GiB device copy that copy_bandwidth() performs
-    (__amd_rocclr_copyBuffer), so that request-size conventions of the counters
-    cancel out.  Writes the record bench.py reads as roofline.traffic.
+    counter reads for the streaming probe's one-read-one-write kernel over 4 GiB
+    (stream_kernel<1, ...>: exactly 4 GiB read and 4 GiB written), so that the
+    request-size conventions of the counters cancel out.  Writes the record that
+    bench.py reads as roofline.traffic.
     """
     import csv
 
@@ -102,49 +135,168 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str, out_path: str):
             return list(csv.DictReader(f))
 
     copy_kib = (4 << 30) / 1024
+    pattern = TRAFFIC_KERNELS[key]
+    pat = re.compile(pattern)
 
-    def per_launch(rows, kernel):
-        # the inference backward only (template arguments: core (lmax, parity),
-        # U, the training flag false, then the waves per center), not the
-        # training variant
-        pat = re.compile(kernel + r"<TPCore<\d+,\s*(true|false)>,\s*\d+,\s*false(,\s*\d+)?>")
+    def per_launch(rows):
         vals = [float(r["Counter_Value"]) for r in rows if pat.search(r["Kernel_Name"])]
         return sum(vals) / len(vals), len(vals)
 
+    def calibration(rows):
+        vals = [float(r["Counter_Value"]) for r in rows if "stream_kernel<1" in r["Kernel_Name"]]
+        return float(np.median(vals))
+
     fr, wr = read(fetch_csv), read(write_csv)
-    f_copy = max(float(r["Counter_Value"]) for r in fr if "copyBuffer" in r["Kernel_Name"])
-    w_copy = max(float(r["Counter_Value"]) for r in wr if "copyBuffer" in r["Kernel_Name"])
-    f_b, n_f = per_launch(fr, "tp_backward_kernel")
-    w_b, _ = per_launch(wr, "tp_backward_kernel")
+    f_cal, w_cal = calibration(fr), calibration(wr)
+    f_b, n_f = per_launch(fr)
+    w_b, _ = per_launch(wr)
     graph = workloads.make_graph(workload)
-    algo = algorithmic_bytes(graph.config, graph.n_atoms, graph.n_edges)["tp_backward"]
-    traffic = (f_b * copy_kib / f_copy + w_b * copy_kib / w_copy) * 1024
-    rec = {"workload": workload, "kernel": "tp_backward", "kernel_source_digest": kernel_source_digest(),
+    cfg = graph.config
+    if key == "tp_mfma_bwd":
+        algo = mfma_bwd_bytes(cfg, graph.n_atoms, graph.n_edges)
+    else:
+        algo = algorithmic_bytes(cfg, graph.n_atoms, graph.n_edges)[key]
+    traffic = (f_b * copy_kib / f_cal + w_b * copy_kib / w_cal) * 1024
+    rec = {"workload": workload, "kernel": key, "kernel_pattern": pattern,
+           "kernel_source_digest": kernel_source_digest(),
            "fetch_kib_per_dispatch": f_b, "write_kib_per_dispatch": w_b, "dispatches": n_f,
-           "copy_calibration": {"copy_bytes": 4 << 30, "fetch_kib": f_copy, "write_kib": w_copy,
-                                "fetch_scale": copy_kib / f_copy, "write_scale": copy_kib / w_copy},
+           "calibration": {"kernel": "stream_kernel<1> (4 GiB read, 4 GiB written)", "fetch_kib": f_cal,
+                           "write_kib": w_cal, "fetch_scale": copy_kib / f_cal, "write_scale": copy_kib / w_cal},
            "traffic_bytes_per_launch": traffic, "algorithmic_bytes_per_launch": algo,
            "traffic_over_algorithmic": traffic / algo}
-    with open(out_path, "w") as f:
+    with open(traffic_record_path(key, workload), "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
 
 
-def copy_bandwidth(torch, dev, n_bytes=4 << 30, reps=10):
-    src = torch.empty(n_bytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
-    dst = torch.empty_like(src)
-    dst.copy_(src)
+# ------------------------------------------------------------------ probes
+
+def stream_probes(torch, dev, n_bytes=4 << 30, reps=5):
+    """Rates (GB/s of bytes moved) of plain streams over 4 GiB per tensor, outside
+    every cache: read only, one read + one write, two reads + one write, each the
+    best over a few launch shapes of the committed probe kernels
+    (csrc/stream_probe.hip: non-temporal 16-byte accesses)."""
+    import ctypes
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2504_16068_amd", "libstream_probe.so"))
+    lib.stream_probe.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_uint, ctypes.c_void_p, ctypes.c_void_p,
+                                 ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]
+    n_f4 = n_bytes // 16
+    a = torch.empty(n_bytes // 4, device=dev).fill_(1.0)
+    b = torch.empty_like(a).fill_(2.0)
+    c = torch.empty_like(a)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    out = {}
+    for pattern, name, tensors in ((0, "read", 1), (1, "read1_write1", 2), (2, "read2_write1", 3)):
+        best = None
+        for unroll in (1, 2, 4):
+            for blocks in (cus * 8, cus * 32, -(-n_f4 // (256 * unroll))):
+                def call():
+                    rc = lib.stream_probe(pattern, unroll, blocks, a.data_ptr(), b.data_ptr(), c.data_ptr(), n_f4,
+                                          stream)
+                    if rc != 0:
+                        raise RuntimeError(f"stream_probe failed ({rc})")
+                call()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    call()
+                e1.record()
+                torch.cuda.synchronize()
+                gbps = tensors * n_bytes / (e0.elapsed_time(e1) / reps / 1e3) / 1e9
+                if best is None or gbps > best["GBps"]:
+                    best = {"GBps": gbps, "unroll": unroll, "blocks": blocks}
+        out[name] = best
+    del a, b, c
+    torch.cuda.empty_cache()
+    return out
+
+
+# the access pattern of each call, for its probe fraction
+PATTERN = {"env_embed": "read", "tp_forward": "read1_write1", "tp_backward": "read2_write1"}
+
+
+# ------------------------------------------------------------- the step
+
+def time_step(torch, at, dev, name, steps, warmup, with_training=True):
+    """Time the hot path (env_embed, tp_forward, tp_backward) on one workload: the
+    wall time of `steps` steps between synchronisations, and each call's mean
+    duration from HIP events on the library's stream."""
+    graph = workloads.make_graph(name)
+    cfg = graph.config
+    n_atoms, n_edges = graph.n_atoms, graph.n_edges
+    if cfg.host_features:
+        xh, wh, _, gh = workloads.host_features(cfg, n_edges)
+        x, w, g = (torch.from_numpy(a).to(dev) for a in (xh, wh, gh))
+    else:
+        x, w, g = workloads.device_features(cfg, n_edges, dev)
+    pw = torch.from_numpy(workloads.path_weights(cfg)).to(dev)
+    rp = torch.from_numpy(graph.row_ptr).to(dev)
+    y = torch.from_numpy(graph.Y).to(dev)
+    plan = at.allegro_tp_plan_create(cfg.lmax, cfg.U, at.ALLEGRO_FULL_PARITY if cfg.full_parity else 0)
+    env = torch.empty((n_atoms, cfg.U, plan.d2), device=dev)
+    out = torch.empty_like(x)
+    grads = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(y))
+
+    def step():
+        at.allegro_env_embed(plan, rp, w, y, env=env)
+        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
+        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
+
+    for _ in range(warmup):
+        step()
     torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for k in range(steps):
+        ev[k][0].record()
+        at.allegro_env_embed(plan, rp, w, y, env=env)
+        ev[k][1].record()
+        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
+        ev[k][2].record()
+        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
+        ev[k][3].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    names = ("env_embed", "tp_forward", "tp_backward")
+    kernel_ms = {nm: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(steps)]))
+                 for i, nm in enumerate(names)}
+    algo = algorithmic_bytes(cfg, n_atoms, n_edges)
+    res = {"graph": graph, "cfg": cfg, "plan": plan, "n_atoms": n_atoms, "n_edges": n_edges,
+           "ms_per_step": wall * 1e3 / steps, "kernel_ms": kernel_ms,
+           "step_event_ms": float(np.mean([ev[k][0].elapsed_time(ev[k][3]) for k in range(steps)])),
+           "algo": algo,
+           "hbm_algorithmic_GBps": {nm: algo[nm] / (kernel_ms[nm] / 1e3) / 1e9 for nm in names}}
+    if with_training:
+        res["training_backward"] = time_training_backward(torch, at, plan, (rp, x, env, pw, g, w, y), grads,
+                                                          kernel_ms, steps)
+    res["tensors"] = (rp, x, env, pw, g, w, y, out, grads)
+    return res
+
+
+def time_training_backward(torch, at, plan, inputs, grads, per_kernel_ms, reps):
+    """The training backward (also grad_path_w), timed outside the step: the
+    whole call, and the extra time over the inference backward."""
+    rp, x, env, pw, g, w, y = inputs
+    ws = torch.empty(at.allegro_tp_backward_workspace(plan, rp.numel() - 1), dtype=torch.uint8, device=x.device)
+    outs = (*grads, torch.empty_like(pw))
+
+    def call():
+        at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, outs=outs, workspace=ws)
+
+    call()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
     for _ in range(reps):
-        dst.copy_(src)
+        call()
     b.record()
     torch.cuda.synchronize()
-    sec = a.elapsed_time(b) / 1e3 / reps
-    del src, dst
-    torch.cuda.empty_cache()
-    return 2 * n_bytes / sec / 1e9
+    ms = a.elapsed_time(b) / reps
+    del ws
+    return {"ms": ms, "extra_over_backward_ms": ms - per_kernel_ms["tp_backward"],
+            "workspace_bytes": at.allegro_tp_backward_workspace(plan, rp.numel() - 1)}
 
 
 def time_harmonics(torch, at, plan, graph, dev, reps):
@@ -176,28 +328,15 @@ def time_harmonics(torch, at, plan, graph, dev, reps):
     return res
 
 
-def time_training_backward(torch, at, plan, inputs, grads, per_kernel_ms, reps):
-    """The training backward (also grad_path_w), timed outside the step: the
-    whole call, and the extra time over the inference backward."""
-    rp, x, env, pw, g, w, y = inputs
-    ws = torch.empty(at.allegro_tp_backward_workspace(plan, rp.numel() - 1), dtype=torch.uint8, device=x.device)
-    outs = (*grads, torch.empty_like(pw))
+def roofline(kernel, algo_bytes, ms, probes, traffic):
+    achieved = algo_bytes / (ms / 1e3) / 1e9
+    probe = probes[PATTERN[kernel]]["GBps"]
+    return {"kernel": kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic, "algorithmic_bytes_per_launch": algo_bytes,
+            "probe_pattern": PATTERN[kernel], "probe_GBps": probe, "frac_of_probe": achieved / probe}
 
-    def call():
-        at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, outs=outs, workspace=ws)
 
-    call()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
-        call()
-    b.record()
-    torch.cuda.synchronize()
-    ms = a.elapsed_time(b) / reps
-    del ws
-    return {"ms": ms, "extra_over_backward_ms": ms - per_kernel_ms["tp_backward"],
-            "workspace_bytes": at.allegro_tp_backward_workspace(plan, rp.numel() - 1)}
-
+# ------------------------------------------------------------------- layer
 
 def layer_algorithmic_bytes(cfg, n_edges: int):
     """Least bytes one layer must move: every input read once, every output written once.
@@ -264,57 +403,99 @@ def time_layer(torch, at, dev, reps, name="medium_layer"):
     return res
 
 
-def cpu_baseline(graph, host_inputs, edges_per_thread=24576, max_threads=16):
-    """Time the fp64 oracle on a prefix of whole center segments of the workload.
+# ------------------------------------------------------------ CPU baseline
 
-    One Python thread per host core (at most max_threads, the host share of one
-    GPU), each running env_embed + forward + backward on its own range of
-    whole segments with single-threaded BLAS; NumPy releases the GIL inside its
-    array loops, so the threads run in parallel.  The single-thread rate on the
-    first range is reported beside it.
-    """
-    from concurrent.futures import ThreadPoolExecutor
+_CPU_JOB = {}
 
+
+def _cpu_range(rng):
+    """One share of the oracle's work: env_embed + forward + backward (fp64 NumPy,
+    single-threaded BLAS) on the centers [c0, c1) of the sample in _CPU_JOB."""
     from threadpoolctl import threadpool_limits
 
     from oracle import tp as otp
 
-    cfg = graph.config
-    threads = max(1, min(max_threads, len(os.sched_getaffinity(0))))
-    n_end = workloads.segment_prefix(graph.row_ptr, threads * edges_per_thread)
-    e_end = int(graph.row_ptr[n_end])
-    x, w, pw, g = host_inputs(e_end)
-    cuts = [0]
-    for k in range(1, threads):
-        cuts.append(max(cuts[-1], workloads.segment_prefix(graph.row_ptr, k * edges_per_thread)))
-    cuts.append(n_end)
-    t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
-
-    def run(k):
-        c0, c1 = cuts[k], cuts[k + 1]
-        s, e = int(graph.row_ptr[c0]), int(graph.row_ptr[c1])
-        if e == s:
-            return 0
-        rp = graph.row_ptr[c0:c1 + 1] - s
-        env = otp.env_embed(rp, w[s:e], graph.Y[s:e])
-        t.forward(rp, x[s:e], env, pw)
-        t.backward(rp, x[s:e], env, pw, g[s:e], w[s:e], graph.Y[s:e])
-        return e - s
-
+    c0, c1 = rng
+    d = _CPU_JOB
+    rp = d["row_ptr"]
+    s, e = int(rp[c0]), int(rp[c1])
+    if e == s:
+        return 0
+    local = rp[c0:c1 + 1] - s
     with threadpool_limits(1):
-        t0 = time.perf_counter()
-        e_single = run(0)
-        sec_single = time.perf_counter() - t0
-        with ThreadPoolExecutor(threads) as ex:
+        env = otp.env_embed(local, d["w"][s:e], d["Y"][s:e])
+        d["tp"].forward(local, d["x"][s:e], env, d["pw"])
+        d["tp"].backward(local, d["x"][s:e], env, d["pw"], d["g"][s:e], d["w"][s:e], d["Y"][s:e])
+    return e - s
+
+
+# (workload, edges of the multi-process sample (None: the whole workload), edges of the single-process sample)
+CPU_SAMPLES = (("small", None, 4096), ("headline", 1 << 18, 4096), ("high_order", 1 << 15, 1024))
+
+
+def cpu_baseline(reps=3):
+    """The fp64 oracle (env_embed + forward + backward) timed on the host, before the
+    GPU is used: on each workload of CPU_SAMPLES, whole center segments split into
+    one range per process over every core of the affinity mask (at most the host
+    share of one GPU), and a smaller prefix in a single process; best of `reps`
+    time.perf_counter runs each.  The small workload's inputs are the GPU run's own;
+    headline and high-order, whose GPU inputs are drawn on the device, use host
+    draws of the same distributions."""
+    import multiprocessing as mp
+
+    from oracle import tp as otp
+
+    affinity = len(os.sched_getaffinity(0))
+    procs = max(1, min(affinity, HOST_SHARE))
+    ctx = mp.get_context("fork")  # the GPU is not initialised yet
+    per = {}
+    for name, multi_edges, single_edges in CPU_SAMPLES:
+        graph = workloads.make_graph(name)
+        cfg = graph.config
+        rp = graph.row_ptr
+        n_multi = graph.n_atoms if multi_edges is None else workloads.segment_prefix(rp, multi_edges)
+        e_multi = int(rp[n_multi])
+        x, w, pw, g = workloads.host_features(cfg, e_multi)
+        _CPU_JOB.clear()
+        _CPU_JOB.update(row_ptr=rp[:n_multi + 1], x=x, w=w, Y=graph.Y[:e_multi], pw=pw, g=g,
+                        tp=otp.TensorProduct(cfg.lmax, cfg.full_parity))
+        cuts = [0]
+        for k in range(1, procs):
+            cuts.append(max(cuts[-1], workloads.segment_prefix(rp[:n_multi + 1], k * e_multi // procs)))
+        cuts.append(n_multi)
+        ranges = [(a, b) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
+        multi = float("inf")
+        with ctx.Pool(procs) as pool:
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                done = sum(pool.map(_cpu_range, ranges, chunksize=1))
+                multi = min(multi, time.perf_counter() - t0)
+        n_single = workloads.segment_prefix(rp, single_edges)
+        e_single = int(rp[n_single])
+        single = float("inf")
+        for _ in range(reps):
             t0 = time.perf_counter()
-            done = sum(ex.map(run, range(threads)))
-            sec = time.perf_counter() - t0
-    return {"value": done / sec, "unit": "edges/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {n_end} centers ({done} edges) of the same workload in {threads} ranges of whole "
-                      f"segments, one Python thread each: env_embed + forward + backward, fp64 NumPy with "
-                      f"single-threaded BLAS, {sec:.1f} s wall",
-            "single_thread_value": e_single / sec_single,
-            "single_thread_sample": f"first {cuts[1]} centers ({e_single} edges), {sec_single:.1f} s"}
+            _cpu_range((0, n_single))
+            single = min(single, time.perf_counter() - t0)
+        per[name] = {"edges_per_s": done / multi, "processes": procs, "sample_edges": done,
+                     "sample_centers": n_multi, "seconds": multi,
+                     "single_process_edges_per_s": e_single / single, "single_sample_edges": e_single}
+        _CPU_JOB.clear()
+    head = per["headline"]
+    return {"value": head["edges_per_s"], "unit": "edges/s", "cores": procs, "affinity_cores": affinity,
+            "kind": "oracle",
+            "sample": f"headline: first {head['sample_centers']} centers ({head['sample_edges']} edges) in "
+                      f"{procs} ranges of whole segments, one process each (fork, before GPU use): env_embed + "
+                      f"forward + backward, fp64 NumPy with single-threaded BLAS, best of {reps}; host-drawn "
+                      f"features of the same distributions",
+            "per_workload": per}
+
+
+# -------------------------------------------------------------------- main
+
+def note(msg):
+    """A progress line on stderr (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def main():
@@ -325,18 +506,24 @@ def main():
     ap.add_argument("--workload", default="headline", choices=sorted(workloads.CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-layer", action="store_true", help="skip the Allegro layer timing")
+    ap.add_argument("--no-high-order", action="store_true", help="skip the high-order record")
     ap.add_argument("--layer-only", action="store_true",
                     help="time only the Allegro layer and print its record (no step, no JSON bench line)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="write the calibrated tp_backward traffic record from two rocprofv3 --pmc runs and exit")
+                    help="write a calibrated traffic record from two rocprofv3 --pmc runs and exit")
+    ap.add_argument("--pmc-kernel", default="tp_backward", choices=sorted(TRAFFIC_KERNELS))
     args = ap.parse_args()
     if args.pmc_summary:
-        pmc_summary(*args.pmc_summary, args.workload, PROFILE_TRAFFIC)
+        pmc_summary(*args.pmc_summary, args.workload, args.pmc_kernel)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the tensor product shards by center ranges with no "
               "communication inside the path; each GPU would run this on its own share.", file=sys.stderr)
         sys.exit(2)
+
+    cpu = None if args.no_cpu_baseline or args.layer_only else cpu_baseline()
+    if cpu is not None:
+        note(f"cpu baseline done: {cpu['value']:.3g} edges/s on {cpu['cores']} processes")
 
     import torch
 
@@ -346,67 +533,22 @@ def main():
     if args.layer_only:
         print(json.dumps({"allegro_layer": time_layer(torch, at, dev, max(3, min(args.steps, 10)))}), flush=True)
         return
-    graph = workloads.make_graph(args.workload)
-    cfg = graph.config
-    n_atoms, n_edges = graph.n_atoms, graph.n_edges
-    if cfg.host_features:
-        xh, wh, pwh, gh = workloads.host_features(cfg, n_edges)
-        x, w, g = (torch.from_numpy(a).to(dev) for a in (xh, wh, gh))
-    else:
-        x, w, g = workloads.device_features(cfg, n_edges, dev)
-    pw = torch.from_numpy(workloads.path_weights(cfg)).to(dev)
-    rp = torch.from_numpy(graph.row_ptr).to(dev)
-    y = torch.from_numpy(graph.Y).to(dev)
-    plan = at.allegro_tp_plan_create(cfg.lmax, cfg.U, at.ALLEGRO_FULL_PARITY if cfg.full_parity else 0)
-    env = torch.empty((n_atoms, cfg.U, plan.d2), device=dev)
-    out = torch.empty_like(x)
-    grads = (torch.empty_like(x), torch.empty_like(env), torch.empty_like(w), torch.empty_like(y))
-
-    def step():
-        at.allegro_env_embed(plan, rp, w, y, env=env)
-        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
-        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for k in range(args.steps):
-        ev[k][0].record()
-        at.allegro_env_embed(plan, rp, w, y, env=env)
-        ev[k][1].record()
-        at.allegro_tp_forward(plan, rp, x, env, pw, out=out)
-        ev[k][2].record()
-        at.allegro_tp_backward(plan, rp, x, env, pw, g, w, y, outs=grads)
-        ev[k][3].record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-
-    names = ("env_embed", "tp_forward", "tp_backward")
-    per_kernel_ms = {nm: float(np.mean([ev[k][i].elapsed_time(ev[k][i + 1]) for k in range(args.steps)]))
-                     for i, nm in enumerate(names)}
-    ms_per_step = wall * 1e3 / args.steps
-    value = n_edges / (ms_per_step / 1e3)
-
+    probes = stream_probes(torch, dev)
+    note("stream probes done: " + ", ".join(f"{k} {v['GBps']:.0f} GB/s" for k, v in probes.items()))
+    st = time_step(torch, at, dev, args.workload, args.steps, args.warmup)
+    note(f"{args.workload} step done: {st['ms_per_step']:.3f} ms")
+    cfg, plan, graph = st["cfg"], st["plan"], st["graph"]
+    n_atoms, n_edges = st["n_atoms"], st["n_edges"]
     harmonics = time_harmonics(torch, at, plan, graph, dev, args.steps)
-    training = time_training_backward(torch, at, plan, (rp, x, env, pw, g, w, y), grads, per_kernel_ms, args.steps)
-    algo = algorithmic_bytes(cfg, n_atoms, n_edges)
-    bwd_s = per_kernel_ms["tp_backward"] / 1e3
-    achieved = algo["tp_backward"] / bwd_s / 1e9
-    copy_gbps = copy_bandwidth(torch, dev)
-    traffic = measured_traffic(args.workload)
-
+    km, algo = st["kernel_ms"], st["algo"]
     result = {
         "metric": METRIC,
-        "value": value,
+        "value": n_edges / (st["ms_per_step"] / 1e3),
         "unit": "edges/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": st["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -419,42 +561,39 @@ def main():
             "atoms": n_atoms, "edges": n_edges, "U": cfg.U, "lmax": cfg.lmax,
             "parity": "full" if cfg.full_parity else "natural", "paths": plan.n_paths, "cg_nnz": plan.nnz,
         },
-        "kernel_ms": per_kernel_ms,
-        "step_event_ms": float(np.mean([ev[k][0].elapsed_time(ev[k][3]) for k in range(args.steps)])),
-        "hbm_algorithmic_GBps": {nm: algo[nm] / (per_kernel_ms[nm] / 1e3) / 1e9 for nm in names},
-        "copy_GBps_measured": copy_gbps,
-        "roofline": {
-            "kernel": "tp_backward",
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": algo["tp_backward"],
-            "frac_of_measured_copy": achieved / copy_gbps,
-        },
+        "kernel_ms": km,
+        "step_event_ms": st["step_event_ms"],
+        "hbm_algorithmic_GBps": st["hbm_algorithmic_GBps"],
+        "frac_of_probe": {nm: st["hbm_algorithmic_GBps"][nm] / probes[PATTERN[nm]]["GBps"] for nm in km},
+        "roofline": roofline("tp_backward", algo["tp_backward"], km["tp_backward"], probes,
+                             measured_traffic("tp_backward", args.workload)),
+        "stream_probes": probes,
         "edge_harmonics": harmonics,
-        "training_backward": training,
+        "training_backward": st["training_backward"],
         "kernel_source_digest": kernel_source_digest(),
     }
-    del x, w, g, out, grads, env
+    del st
     torch.cuda.empty_cache()
+    if not args.no_high_order and args.workload != "high_order":
+        ho = time_step(torch, at, dev, "high_order", min(args.steps, 10), args.warmup)
+        note(f"high_order step done: {ho['ms_per_step']:.3f} ms")
+        hk, ha = ho["kernel_ms"], ho["algo"]
+        result["high_order"] = {
+            "workload": f"high_order: {ho['n_atoms']} atoms, cutoff {ho['cfg'].cutoff} A, {ho['n_edges']} edges, "
+                        f"U={ho['cfg'].U}, lmax={ho['cfg'].lmax}, full parity",
+            "ms_per_step": ho["ms_per_step"], "edges_per_s": ho["n_edges"] / (ho["ms_per_step"] / 1e3),
+            "kernel_ms": hk, "hbm_algorithmic_GBps": ho["hbm_algorithmic_GBps"],
+            "frac_of_probe": {nm: ho["hbm_algorithmic_GBps"][nm] / probes[PATTERN[nm]]["GBps"] for nm in hk},
+            "roofline": roofline("tp_backward", ha["tp_backward"], hk["tp_backward"], probes,
+                                 measured_traffic("tp_backward", "high_order")),
+            "training_backward": ho["training_backward"]}
+        del ho
+        torch.cuda.empty_cache()
     if not args.no_layer:
         result["allegro_layer"] = time_layer(torch, at, dev, max(3, min(args.steps, 10)))
-    if not args.no_cpu_baseline:
-        cfg_ = cfg
-
-        def host_inputs(e):
-            if cfg_.host_features:
-                return xh[:e], wh[:e], pwh, gh[:e]
-            xs, ws, gs = workloads.device_features(cfg_, n_edges, dev)
-            res = xs[:e].cpu().numpy(), ws[:e].cpu().numpy(), workloads.path_weights(cfg_), gs[:e].cpu().numpy()
-            del xs, ws, gs
-            torch.cuda.empty_cache()
-            return res
-
-        result["cpu_baseline"] = cpu_baseline(graph, host_inputs)
+        note("layer done")
+    if cpu is not None:
+        result["cpu_baseline"] = cpu
     print(json.dumps(result), flush=True)
 
 

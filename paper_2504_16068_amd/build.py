@@ -6,7 +6,8 @@ Steps (every call rebuilds everything):
   2. g++ compiles the builder for the library (host code, -fPIC);
   3. hipcc compiles the kernels and the C ABI for gfx950 (the tensor product,
      then the layer around it), with packed-fp32 instruction selection disabled;
-  4. hipcc links liballegro_tp.so next to this file.
+  4. hipcc links liballegro_tp.so next to this file, and builds bench.py's
+     streaming probes (libstream_probe.so, not part of the ABI).
 The per-kernel register / scratch report of step 3 is written to
 _build/resource_usage.txt; a kernel that spills to scratch fails the build.
 """
@@ -25,6 +26,7 @@ CSRC = os.path.join(PKG, "csrc")
 GEN = os.path.join(CSRC, "generated")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liballegro_tp.so")
+PROBE_LIB = os.path.join(PKG, "libstream_probe.so")  # bench.py's streaming probes, outside the ABI
 ARCH = "gfx950"
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 HIP_SOURCES = ("allegro_tp.hip", "allegro_layer.hip")  # tensor product; the layer around it
@@ -88,6 +90,9 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, cg_obj, "-o", tmp])
     os.replace(tmp, LIB)
+    tmp = PROBE_LIB + ".tmp"
+    _run([HIPCC, *HIP_FLAGS, "-shared", os.path.join(CSRC, "stream_probe.hip"), "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
     if verbose:
         print(summary)
     return LIB

@@ -65,29 +65,79 @@ def _write_counters(path, rows):
 
 
 def test_pmc_summary_calibrates_and_selects_the_inference_backward(tmp_path, monkeypatch):
-    """Each counter is scaled by what it reads for the 4 GiB copy; only the inference
-    backward's dispatches (template flag false) are averaged, not the training ones."""
+    """Each counter is scaled by what it reads for the 4 GiB one-read-one-write
+    probe; only the inference backward's dispatches (template flag false) are
+    averaged, not the training ones."""
     copy_kib = (4 << 30) / 1024
     inf = "void (anonymous namespace)::tp_backward_kernel<TPCore<1, false>, 16, false, 16>(long const*)"
     train = "void (anonymous namespace)::tp_backward_kernel<TPCore<1, false>, 16, true, 4>(long const*)"
+    probe = "void (anonymous namespace)::stream_kernel<1, 4>(float const*)"
+    probe_read = "void (anonymous namespace)::stream_kernel<0, 4>(float const*)"
     fetch = tmp_path / "fetch.csv"
     write = tmp_path / "write.csv"
-    # fetch counts half of the copy's bytes, write all of them
-    _write_counters(fetch, [("__amd_rocclr_copyBuffer", copy_kib / 2), (inf, 100.0), (inf, 300.0), (train, 1e9)])
-    _write_counters(write, [("__amd_rocclr_copyBuffer", copy_kib), (inf, 50.0), (inf, 50.0), (train, 1e9)])
-    out = tmp_path / "traffic.json"
-    bench.pmc_summary(str(fetch), str(write), "tiny", str(out))
+    # fetch counts half of the probe's bytes, write all of them
+    _write_counters(fetch, [(probe, copy_kib / 2), (probe, copy_kib / 2), (probe_read, 1.0), (inf, 100.0),
+                            (inf, 300.0), (train, 1e9)])
+    _write_counters(write, [(probe, copy_kib), (probe, copy_kib), (probe_read, 5.0), (inf, 50.0), (inf, 50.0),
+                            (train, 1e9)])
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    bench.pmc_summary(str(fetch), str(write), "tiny", "tp_backward")
+    out = tmp_path / "tp_backward_tiny_traffic.json"
     rec = json.loads(out.read_text())
     assert rec["dispatches"] == 2
     assert rec["fetch_kib_per_dispatch"] == 200.0 and rec["write_kib_per_dispatch"] == 50.0
-    assert rec["copy_calibration"]["fetch_scale"] == 2.0 and rec["copy_calibration"]["write_scale"] == 1.0
+    assert rec["calibration"]["fetch_scale"] == 2.0 and rec["calibration"]["write_scale"] == 1.0
     assert rec["traffic_bytes_per_launch"] == (200.0 * 2 + 50.0) * 1024
     g = workloads.make_graph("tiny")
     assert rec["algorithmic_bytes_per_launch"] == bench.algorithmic_bytes(g.config, g.n_atoms, g.n_edges)["tp_backward"]
     # the record is used only while the kernel sources and the workload match
-    monkeypatch.setattr(bench, "PROFILE_TRAFFIC", str(out))
-    assert bench.measured_traffic("tiny") == rec["traffic_bytes_per_launch"]
-    assert bench.measured_traffic("headline") is None
+    assert bench.measured_traffic("tp_backward", "tiny") == rec["traffic_bytes_per_launch"]
+    assert bench.measured_traffic("tp_backward", "headline") is None
     rec["kernel_source_digest"] = "0" * 16
     out.write_text(json.dumps(rec))
-    assert bench.measured_traffic("tiny") is None
+    assert bench.measured_traffic("tp_backward", "tiny") is None
+
+
+def test_pmc_patterns_select_their_kernels():
+    import re
+    names = {
+        "tp_backward": ["void (anonymous namespace)::tp_backward_kernel<TPCore<2, true>, 64, false, 16>(long const*)",
+                        "void (anonymous namespace)::tp_backward_kernel<TPCore<3, true>, 128, false, 8>(long const*)"],
+        "tp_forward": ["void (anonymous namespace)::tp_forward_kernel<TPCore<2, true>, 64, 16>(long const*)",
+                       "void (anonymous namespace)::tp_matrix_kernel<TPCore<3, true>, 128, TPMFwd<3, true> >(long)"],
+        "tp_mfma_bwd": ["void (anonymous namespace)::tp_mfma_bwd_kernel<true, 128, true>(long, long const*)"],
+    }
+    for key, pattern in bench.TRAFFIC_KERNELS.items():
+        for other, kernels in names.items():
+            for name in kernels:
+                assert bool(re.search(pattern, name)) == (key == other), (key, other, name)
+    # the training backward at lmax <= 2 and the backward's grad_x matrix kernel are not selected
+    for pattern in bench.TRAFFIC_KERNELS.values():
+        assert not re.search(pattern, "void (anonymous namespace)::tp_backward_kernel<TPCore<2, true>, 64, true, 4>(long)")
+        assert not re.search(pattern, "void (anonymous namespace)::tp_matrix_kernel<TPCore<3, true>, 64, "
+                                      "TPMBwdX<3, true> >(long)")
+
+
+def test_mfma_bwd_bytes():
+    g = workloads.make_graph("tiny")
+    cfg = workloads.CONFIGS["high_order"]
+    d1, d2, P = workloads.dims(cfg.lmax, cfg.full_parity)
+    N, E = 10, 1000
+    assert bench.mfma_bwd_bytes(cfg, N, E) == (4 * (3 * E * cfg.U * d1 + 2 * N * cfg.U * d2 + N * P * cfg.U)
+                                               + (N + 1) * 8 + 4 * P * cfg.U)
+    del g
+
+
+def test_cpu_baseline_ranges_cover_the_sample():
+    """The oracle's per-process ranges run every center of the sample exactly once."""
+    g = workloads.make_graph("tiny")
+    x, w, pw, gr = workloads.host_features(g.config, g.n_edges)
+    from oracle import tp as otp
+    bench._CPU_JOB.update(row_ptr=g.row_ptr, x=x, w=w, Y=g.Y, pw=pw, g=gr,
+                          tp=otp.TensorProduct(g.config.lmax, g.config.full_parity))
+    try:
+        n = g.n_atoms
+        assert bench._cpu_range((0, n)) == g.n_edges
+        assert bench._cpu_range((0, 10)) + bench._cpu_range((10, n)) == g.n_edges
+    finally:
+        bench._CPU_JOB.clear()
