@@ -99,6 +99,48 @@ def test_layer_small_workload(at):
     _compare(lay, (_np(h_o), _np(V_o), _host(g)), ref, "layer_small")
 
 
+def test_two_stacked_layers(at):
+    """Two layers in sequence on layer_small (the paper's model stacks layers, each
+    taking the previous one's (h, V) and the same edge harmonics Y, Table I):
+    the second layer's output and, through both backwards chained on the device,
+    the input gradients, dY (summed over both layers) and every weight gradient
+    of both layers against the oracle chained in fp64."""
+    import dataclasses
+
+    graph = workloads.make_graph("layer_small")
+    cfg = graph.config
+    L, H = cfg.extra["L"], cfg.extra["H"]
+    prm1 = workloads.layer_params(cfg)
+    prm2 = workloads.layer_params(dataclasses.replace(cfg, index=cfg.index + 1000))
+    h, V, dh_out, dV_out = workloads.layer_inputs(cfg, graph.n_edges)
+    _note(f"[gpu] two stacked layers on layer_small: N={graph.n_atoms} E={graph.n_edges}")
+    plan = _plan(at, cfg.lmax, cfg.full_parity)
+    rp, Yd = _t(graph.row_ptr), _t(graph.Y)
+    w1, w2 = ({k: _t(v) for k, v in p.items()} for p in (prm1, prm2))
+    h1, V1, saved1 = at.allegro_layer_forward(plan, L, H, rp, _t(h), _t(V), Yd, w1)
+    h2, V2, saved2 = at.allegro_layer_forward(plan, L, H, rp, h1, V1, Yd, w2)
+    g2 = at.allegro_layer_backward(plan, L, H, rp, h1, V1, Yd, w2, saved2, _t(dh_out), _t(dV_out))
+    g1 = at.allegro_layer_backward(plan, L, H, rp, _t(h), _t(V), Yd, w1, saved1, g2["h"], g2["V"])
+    torch.cuda.synchronize()
+
+    lay = olayer.AllegroLayer(cfg.lmax, cfg.full_parity, 64, L, H)
+    rh1, rV1, _ = lay.forward(graph.row_ptr, h, V, graph.Y, prm1)
+    rh2, rV2, _ = lay.forward(graph.row_ptr, rh1, rV1, graph.Y, prm2)
+    rg2 = lay.backward(graph.row_ptr, rh1, rV1, graph.Y, prm2, dh_out, dV_out)
+    rg1 = lay.backward(graph.row_ptr, h, V, graph.Y, prm1, rg2["h"], rg2["V"])
+    xs = lay.tp.x_slices
+    errs = {"h_out": (block_rel_err(_np(h2), rh2), FWD_TOL), "V_out": (block_rel_err(_np(V2), rV2, xs), FWD_TOL),
+            "dh": (block_rel_err(_np(g1["h"]), rg1["h"]), BWD_TOL),
+            "dV": (block_rel_err(_np(g1["V"]), rg1["V"], xs), BWD_TOL),
+            "dY": (block_rel_err(_np(g1["Y"]) + _np(g2["Y"]), rg1["Y"] + rg2["Y"], lay.tp.env_slices), BWD_TOL)}
+    for k in WEIGHTS:
+        errs["d" + k + "1"] = (block_rel_err(_np(g1[k]), rg1[k]), BWD_TOL)
+        errs["d" + k + "2"] = (block_rel_err(_np(g2[k]), rg2[k]), BWD_TOL)
+    _note("two layers: " + ", ".join(f"{k}={v:.2e}" for k, (v, _) in errs.items()))
+    bad = {k: v for k, (v, tol) in errs.items() if not v <= tol}
+    assert not bad, f"two layers: parity failed {bad}"
+
+
 def _synthetic(lmax, full, L, H, degrees, seed):
     rng = np.random.default_rng(seed)
     degrees = np.asarray(degrees, dtype=np.int64)

@@ -523,7 +523,7 @@ def test_scalar_path_weights_broadcast(at):
     assert block_rel_err(got_scalar, ref_scalar) <= BWD_TOL
 
 
-@pytest.mark.parametrize("name", ["headline", "high_order"])
+@pytest.mark.parametrize("name", ["headline", "high_order", "large"])
 def test_deterministic_env_full_size_sampled(at, name, n_samples=32):
     """Deterministic env at full size: sampled centers bit-equal to the fp32 sequential replay."""
     graph = workloads.make_graph(name)
