@@ -17,13 +17,15 @@ HBM peak and against the rate of a plain streaming kernel of the same access
 pattern timed in the same run (stream_probes).  Extra keys:
   high_order      the same step at Table I's large-model shape (lmax 3, 128
                   channels), with its own roofline object;
+  large           the headline step on 100,000 atoms at cutoff 6 A (about 9e6
+                  edges), with its own roofline object;
   allegro_layer   one whole Allegro layer (forward, and backward with every
                   weight gradient) at the medium model shape of Table I;
   cpu_baseline    the fp64 oracle on bounded samples of the small, headline and
                   high-order workloads, timed before the GPU is touched.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline] [--no-layer] [--no-high-order]
+                       [--no-cpu-baseline] [--no-layer] [--no-high-order] [--no-large]
        python bench.py --layer-only
        python bench.py --pmc-summary FETCH_CSV WRITE_CSV --pmc-kernel NAME
                        (after two rocprofv3 --pmc runs; see pmc_summary)
@@ -507,6 +509,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-layer", action="store_true", help="skip the Allegro layer timing")
     ap.add_argument("--no-high-order", action="store_true", help="skip the high-order record")
+    ap.add_argument("--no-large", action="store_true", help="skip the large-system record")
     ap.add_argument("--layer-only", action="store_true",
                     help="time only the Allegro layer and print its record (no step, no JSON bench line)")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -574,20 +577,24 @@ def main():
     }
     del st
     torch.cuda.empty_cache()
-    if not args.no_high_order and args.workload != "high_order":
-        ho = time_step(torch, at, dev, "high_order", min(args.steps, 10), args.warmup)
-        note(f"high_order step done: {ho['ms_per_step']:.3f} ms")
-        hk, ha = ho["kernel_ms"], ho["algo"]
-        result["high_order"] = {
-            "workload": f"high_order: {ho['n_atoms']} atoms, cutoff {ho['cfg'].cutoff} A, {ho['n_edges']} edges, "
-                        f"U={ho['cfg'].U}, lmax={ho['cfg'].lmax}, full parity",
-            "ms_per_step": ho["ms_per_step"], "edges_per_s": ho["n_edges"] / (ho["ms_per_step"] / 1e3),
-            "kernel_ms": hk, "hbm_algorithmic_GBps": ho["hbm_algorithmic_GBps"],
-            "frac_of_probe": {nm: ho["hbm_algorithmic_GBps"][nm] / probes[PATTERN[nm]]["GBps"] for nm in hk},
-            "roofline": roofline("tp_backward", ha["tp_backward"], hk["tp_backward"], probes,
-                                 measured_traffic("tp_backward", "high_order")),
-            "training_backward": ho["training_backward"]}
-        del ho
+    # the other workloads of the paper's Table I shapes: the large model (lmax 3,
+    # 128 channels) and the headline model on a system 5x larger
+    for key, skip, steps in (("high_order", args.no_high_order, 10), ("large", args.no_large, 5)):
+        if skip or args.workload == key:
+            continue
+        ot = time_step(torch, at, dev, key, min(args.steps, steps), args.warmup)
+        note(f"{key} step done: {ot['ms_per_step']:.3f} ms")
+        ok, oa, oc = ot["kernel_ms"], ot["algo"], ot["cfg"]
+        result[key] = {
+            "workload": f"{key}: {ot['n_atoms']} atoms, cutoff {oc.cutoff} A, {ot['n_edges']} edges, "
+                        f"U={oc.U}, lmax={oc.lmax}, {'full' if oc.full_parity else 'natural'} parity",
+            "ms_per_step": ot["ms_per_step"], "edges_per_s": ot["n_edges"] / (ot["ms_per_step"] / 1e3),
+            "kernel_ms": ok, "hbm_algorithmic_GBps": ot["hbm_algorithmic_GBps"],
+            "frac_of_probe": {nm: ot["hbm_algorithmic_GBps"][nm] / probes[PATTERN[nm]]["GBps"] for nm in ok},
+            "roofline": roofline("tp_backward", oa["tp_backward"], ok["tp_backward"], probes,
+                                 measured_traffic("tp_backward", key)),
+            "training_backward": ot["training_backward"]}
+        del ot
         torch.cuda.empty_cache()
     if not args.no_layer:
         result["allegro_layer"] = time_layer(torch, at, dev, max(3, min(args.steps, 10)))

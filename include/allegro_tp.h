@@ -146,8 +146,9 @@ int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t
  *   grad_path_w[p][u] = sum_e sum_{(i,j,k) in p} C_ijk x[e,u,i] env[c(e),u,j] grad_out[e,u,k]
  * (for one scalar weight per path, sum grad_path_w over u).  The sum is
  * deterministic: each center's contribution is summed over its edges in a
- * fixed order and written to workspace rows [N][n_paths][U], which two
- * reduction launches then sum in a fixed order.  The other four gradients
+ * fixed order and written to one workspace row of n_paths * U floats per
+ * center (path-major, or channel-major at lmax 3), which two reduction
+ * launches then sum in a fixed order.  The other four gradients
  * equal allegro_tp_backward's up to fp32 rounding (the two split the work
  * differently; at lmax 3 this call forms grad_x = M^T grad_out with the
  * per-center matrix of the forward).  workspace is caller-owned device memory of at least

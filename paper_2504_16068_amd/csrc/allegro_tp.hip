@@ -478,8 +478,24 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
 }
 
 // ------------------------------------------------- embedding VJP (pass 2)
+// LDS layout of grad_env[n] for the embedding VJP: the U rows of D2 floats in
+// eight groups of U / 8 channels.  With D2 % 4 == 0 the rows are read 16 bytes
+// at a time and each group is padded to a stride of 4 (mod 8) floats, so that
+// the eight lane groups of the grad_Y sums (one channel group each) read
+// distinct banks; unpadded, all eight hit the same bank quad.  Other row
+// lengths (d2 = 9 at lmax 2) keep the plain layout, which measured faster
+// there than an odd stride.
+template <int U, int D2>
+struct GeRows {
+  static constexpr int UQ = U / 8, S0 = UQ * D2;
+  static constexpr int PAD = D2 % 4 == 0 ? (S0 % 8 == 4 ? 0 : 4) : 0;
+  static constexpr int GS = S0 + PAD, FLOATS = 8 * GS;
+  static_assert(U % 8 == 0, "eight channel groups");
+  static constexpr int idx(int u, int j) { return (u / UQ) * GS + (u % UQ) * D2 + j; }
+};
+
 // The embedding's VJP for the edges [e0, e1) of center n, given its complete
-// grad_env[n] rows [U][D2] in LDS (ge_l), in batches of EB edges dealt round
+// grad_env[n] rows in LDS (ge_l, GeRows layout), in batches of EB edges dealt round
 // robin to the NW waves of the center; each wave first stages the batch's w
 // and Y rows in its own LDS area (stage, EB * (U + 1 + D2) floats) with one
 // round of coalesced loads:
@@ -503,7 +519,7 @@ __device__ __forceinline__ void embedding_vjp(const float *ge_l, float *stage, i
 #pragma unroll
   for (int c = 0; c < L::CPL; ++c)
 #pragma unroll
-    for (int j = 0; j < D2; ++j) gel[c][j] = ge_l[(ul + c * kWave) * D2 + j];
+    for (int j = 0; j < D2; ++j) gel[c][j] = ge_l[GeRows<U, D2>::idx(ul + c * kWave, j)];
   for (int64_t eb = e0 + int64_t(wave) * EB; eb < e1; eb += int64_t(NW) * EB) {
     const int cnt = int(e1 - eb < EB ? e1 - eb : EB);
     lds_sync<1>();  // this wave's previous batch is done with its staged rows
@@ -528,7 +544,7 @@ __device__ __forceinline__ void embedding_vjp(const float *ge_l, float *stage, i
       constexpr int UQ = U / 8;  // channels per lane
       const int k = lane / 8, q = lane % 8;
       const float *wrow = wl + k * WROW + q * UQ;
-      const float *gq = ge_l + q * UQ * D2;
+      const float *gq = ge_l + q * GeRows<U, D2>::GS;
       float gy[D2];
 #pragma unroll
       for (int j = 0; j < D2; ++j) gy[j] = 0.0f;
@@ -559,17 +575,20 @@ __global__ __launch_bounds__(kWave * NW) void embedding_vjp_kernel(const int64_t
                                                                    const float *__restrict__ Y,
                                                                    float *__restrict__ grad_w,
                                                                    float *__restrict__ grad_Y) {
+  using GR = GeRows<U, D2>;
   constexpr int EB = 8, STAGE = EB * (U + 1 + D2);
-  __shared__ float4 smem[(U * D2 + NW * STAGE + 3) / 4];
+  static_assert(D2 % 4 == 0 && GR::GS % 4 == 0, "grad_env rows staged 16 bytes at a time");
+  __shared__ float4 smem[(GR::FLOATS + NW * STAGE + 3) / 4];
   float *ge_l = reinterpret_cast<float *>(smem);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
   if (e1 <= e0) return;
   const float4 *src = reinterpret_cast<const float4 *>(grad_env + n * U * D2);
-  for (int i = tid; i < U * D2 / 4; i += kWave * NW) reinterpret_cast<float4 *>(ge_l)[i] = src[i];
+  for (int i = tid; i < U * D2 / 4; i += kWave * NW)
+    *reinterpret_cast<float4 *>(ge_l + GR::idx(4 * i / D2, 4 * i % D2)) = src[i];
   lds_sync<NW>();
-  embedding_vjp<U, D2, NW, EB>(ge_l, ge_l + U * D2 + wave * STAGE, e0, e1, wave, lane, w, Y, grad_w, grad_Y);
+  embedding_vjp<U, D2, NW, EB>(ge_l, ge_l + GR::FLOATS + wave * STAGE, e0, e1, wave, lane, w, Y, grad_w, grad_Y);
 }
 
 // ------------------------------------------------------ tensor product bwd
@@ -623,7 +642,7 @@ struct BwdLds {
   static constexpr int P1 = NW * 2 * TILE_F4 * 4;
   static constexpr int GS = odd_stride(D2);  // row stride of the grad_env partial sums
   static constexpr int GE_PART = NW * kWave * GS;
-  static constexpr int GE_ROW = U * D2;
+  static constexpr int GE_ROW = GeRows<U, D2>::FLOATS;
   static constexpr int STAGE = EB * (WROW + D2);
   static constexpr int P2 = GE_PART + GE_ROW + NW * STAGE;
   static constexpr int PC_FIT = (P1 / (NW * kWave) - 1) | 1;  // odd, and its stride fits in P1
@@ -702,7 +721,7 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
     float a = 0.0f;
     for (int k = 0; k < WPT; ++k)
       for (int q = 0; q < L::G; ++q) a += ge_part[((tt * WPT + k) * kWave + q * L::LPE + uw) * B::GS + j];
-    ge_l[i] = a;
+    ge_l[GeRows<U, D2>::idx(uu, j)] = a;
     grad_env[n * U * D2 + i] = a;
   }
   lds_sync<NW>();
@@ -864,7 +883,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
       }
       if (lane < CPW * D2) grad_env[(fn * U + fu0) * D2 + lane] = 0.0f;
       if constexpr (WG) {
-        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(fn * NP + i / CPW) * U + fu0 + i % CPW] = 0.0f;
+        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(fn * U + fu0) * NP + i] = 0.0f;
       }
       fq += total;
     }
@@ -977,7 +996,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
             const float e = __shfl(pev[cw], int(zp >> 16));
             a = __builtin_fmaf(in ? Hz[off + k] : 0.0f, e, a);
           }
-          if (p < NP) pw_part[(p_n * NP + p) * U + u] = a;
+          if (p < NP) pw_part[(p_n * U + u) * NP + p] = a;  // channel-major row: one contiguous store
         }
       }
     }
@@ -1236,13 +1255,15 @@ __global__ __launch_bounds__(256) void pw_reduce_rows_kernel(int64_t N, int cols
   chunk_sums[int64_t(blockIdx.y) * cols + c] = (a0 + a1) + (a2 + a3);
 }
 
+// With np > 0 the rows are channel-major ([U][np], column c = u np + p) and
+// the sum goes to grad_pw[p][u]; with np == 0 columns map one to one.
 __global__ __launch_bounds__(256) void pw_reduce_chunks_kernel(int rows, int cols, const float *__restrict__ chunk_sums,
-                                                               float *__restrict__ grad_pw) {
+                                                               float *__restrict__ grad_pw, int np) {
   const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
   if (c >= cols) return;
   float a = 0.0f;
   for (int r = 0; r < rows; ++r) a += chunk_sums[int64_t(r) * cols + c];
-  grad_pw[c] = a;
+  grad_pw[np > 0 ? (c % np) * (cols / np) + c / np : c] = a;
 }
 
 __global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restrict__ p) {
@@ -1601,6 +1622,12 @@ int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t
   return ALLEGRO_OK;
 }
 
+// Layout of the per-center path-weight rows the training backward writes:
+// [n_paths][U] (returns 0) from the direct kernels, channel-major [U][n_paths]
+// (returns n_paths) from the matrix-core kernel at lmax 3, where a channel's
+// row is one contiguous store.
+static int pw_rows_np(const allegro_tp_plan *plan) { return plan->lmax >= 3 ? int(plan->table.paths.size()) : 0; }
+
 int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
                               const float *x, const float *env, const float *path_w, const float *grad_out,
                               const float *w, const float *Y, float *grad_x, float *grad_env, float *grad_w,
@@ -1637,7 +1664,8 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
   if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
   const unsigned cb = unsigned((cols + 255) / 256);
   hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
-  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w);
+  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w,
+                     pw_rows_np(plan));
   return after_launch("allegro_tp_backward_train");
 }
 
@@ -1687,11 +1715,11 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
              grad_env + n0 * ud2, grad_w, grad_Y, part);
     hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, n1 - n0, cols, part, ranges);
     hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, ranges,
-                       chunk_rows + c * cols);
+                       chunk_rows + c * cols, 0);
     if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
   }
   hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, int(n_chunks), cols, chunk_rows,
-                     grad_path_w);
+                     grad_path_w, pw_rows_np(plan));
   return after_launch("allegro_tp_backward_train_noalloc");
 }
 

@@ -479,7 +479,12 @@ def test_train_backward_full_size(at, name, n_samples=16):
     env = at.allegro_env_embed(plan, rp, w, yd)
     (gx, _, _, _, gpw), ws = _train(at, plan, rp, x, env, pwd, g, w, yd)
     n, cols = graph.n_atoms, plan.n_paths * cfg.U
-    part = ws[: n * cols * 4].view(torch.float32).view(n, plan.n_paths, cfg.U)
+    rows = ws[: n * cols * 4].view(torch.float32)
+    # a center's row is path-major [P][U], or channel-major [U][P] at lmax 3
+    if cfg.lmax >= 3:
+        part = rows.view(n, cfg.U, plan.n_paths).permute(0, 2, 1)
+    else:
+        part = rows.view(n, plan.n_paths, cfg.U)
     rng = np.random.default_rng(cfg.index + 50)
     centers = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, n_samples)]))
     t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
@@ -493,7 +498,7 @@ def test_train_backward_full_size(at, name, n_samples=16):
         ref_gx = t.backward(local, xs, env_c, pw, gs, ws_, graph.Y[s:e])[0]
         assert block_rel_err(gx[s:e].cpu().numpy(), ref_gx, t.x_slices) <= BWD_TOL, c
     del gx
-    ph = part.cpu().numpy().astype(np.float64).reshape(n, cols)
+    ph = np.ascontiguousarray(part.cpu().numpy()).astype(np.float64).reshape(n, cols)
     total = ph.sum(axis=0)
     # recursive-summation bound: at most ceil(ceil(N / 128) / 4) + 130 sequential fp32 additions
     depth = -(-(-(-n // 128)) // 4) + 130

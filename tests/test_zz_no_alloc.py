@@ -67,7 +67,11 @@ def test_noalloc_matches_workspace_version(lmax, U):
         _note(f"  grad_path_w err vs workspace version {err:.2e}")
         assert err <= BWD_TOL
         # fp64 sum of the per-center rows the workspace version wrote
-        part = ws[: n * cols * 4].view(torch.float32).view(n, cols).cpu().numpy().astype(np.float64)
+        rows = ws[: n * cols * 4].view(torch.float32)
+        # a center's row is path-major [P][U], or channel-major [U][P] at lmax 3
+        if lmax >= 3:
+            rows = rows.view(n, U, plan.n_paths).permute(0, 2, 1)
+        part = np.ascontiguousarray(rows.cpu().numpy()).reshape(n, cols).astype(np.float64)
         total = part.sum(axis=0)
         got_pw = got[4].cpu().numpy().reshape(cols).astype(np.float64)
         # recursive-summation bound: per chunk ceil(ceil(rows / 128) / 4) + 2 additions in a
