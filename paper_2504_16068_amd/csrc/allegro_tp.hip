@@ -747,20 +747,38 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 // (accumulator); the generated tables (TPMfmaTab) build M's cells and contract
 // G's cells lane by lane from the sparse coupling table.
 //
-// Work: every wave walks its own sequence of pairs (center n, CPW consecutive
-// channels), CPW = 32 / d1 so that a pair's row of one edge is 128 contiguous
-// bytes (one channel with full parity, two without), pairs dealt round robin
-// over all waves of the persistent grid (one workgroup of 16 waves per compute
-// unit, sharing one copy of the tables).  A pair's edges move in tiles of 16
-// edges; DEPTH tiles (of this pair and the next ones) are in flight in
-// registers at any time, and the tile being multiplied is staged in the wave's
-// own LDS area (x and g, XOR-swizzled 16-byte columns, so that the row reads of
-// the grad_x operand and the column reads of the G operands are conflict-free).
-// There is no barrier between waves: when a pair's first tile comes up, the
-// wave contracts the previous pair's G (spilled to its LDS area) and builds the
-// new pair's M while its next tiles are still arriving and the other waves keep
-// streaming.  Every sum has a fixed order.  The embedding VJP, which needs all
-// channels of grad_env[n], is embedding_vjp_kernel, launched after this kernel.
+// Work: the pairs (center n, CPW consecutive channels; CPW = 32 / d1, so that a
+// pair's row of one edge is 128 contiguous bytes: one channel with full
+// parity, two without) are dealt round robin to the streaming waves of a
+// persistent grid of one workgroup per compute unit.  Each of the NW
+// streaming waves is paired with a helper wave of its own:
+//   * the streaming wave moves its pairs' edges in tiles of 16 edges, DEPTH
+//     tiles in flight in registers at any time, the tile being multiplied
+//     staged in its LDS area (x and g, XOR-swizzled 16-byte columns, so that
+//     the row reads of the grad_x operand and the column reads of the G
+//     operands are conflict-free), and runs the matrix-core products;
+//   * the helper builds the next pair's M and contracts the previous pair's G
+//     (grad_env and the path-weight rows) from the generated lane tables,
+//     while its streaming wave keeps streaming; it also writes the zero sums of
+//     pairs without edges.  The helper's work is mostly LDS reads, and the
+//     LDS is what it shares with the streaming waves: so it keeps the terms
+//     of M it uses most (the first two of each cell) and its H indices in
+//     registers (10-bit indices, three to a word), issues the loads of the
+//     next pair's path weights and env row before it contracts the previous
+//     pair, and runs at a raised wave priority, since a streaming wave waits
+//     whenever its helper falls behind.
+// They hand M and G over through two LDS buffers of the pair, each guarded by a
+// counter: M_ready / M_taken for M (helper writes pair k's M once the wave has
+// taken pair k - 1's), G_written / G_taken for G (the wave writes pair k's G
+// once the helper has contracted pair k - 1's).  Every wait is bounded; if one
+// ever ran out (it cannot, unless the kernel itself is wrong) every later wait
+// of the workgroup returns at once and the kernel runs to its end with wrong
+// sums.  The streaming wave has no early exit and issues the same memory
+// instructions for every tile: either would make the compiler wait for all of
+// its loads in flight at every tile.  There is no barrier between waves after
+// the tables are loaded.
+// Every sum has a fixed order.  The embedding VJP, which needs all channels
+// of grad_env[n], is embedding_vjp_kernel, launched after this kernel.
 constexpr int kMfmaEdges = 16;  // edges per tile
 
 template <bool FULL>
@@ -773,14 +791,14 @@ struct MfmaShape {
   static constexpr int LR = kWave / RF4;         // rows per 16-byte load instruction
   static constexpr int LJ = kMfmaEdges / LR;     // load instructions per tensor and tile
   static constexpr int TILE = kMfmaEdges * ROW;  // floats of one tensor's tile
-  static constexpr int DEPTH = 3;                // tiles in flight per wave
-  static constexpr int NW = 16, THREADS = kWave * NW;
-  // between tiles a wave's LDS area holds one channel's G spill [S][64] and H or Z
-  static constexpr int GL = S * kWave;
-  static constexpr int HZ = Tab::NZ + 2 > Tab::RZ * kWave ? Tab::NZ + 2 : Tab::RZ * kWave;
-  static constexpr int AREA = (2 * TILE > GL + HZ ? 2 * TILE : GL + HZ + 3) / 4 * 4;
+  static constexpr int DEPTH = 4;                // tiles in flight per streaming wave
+  static constexpr int NW = 8, THREADS = 2 * kWave * NW;  // streaming waves, then their helpers
+  static constexpr int MB = CPW * S * kWave;     // floats of a pair's M (or G) in lane layout
+  static constexpr int HZ = ((Tab::NZ + 2 > Tab::RZ * kWave ? Tab::NZ + 2 : Tab::RZ * kWave) + 3) / 4 * 4;
+  // per streaming wave: tile area, M buffer, G buffer; per helper: Z / H scratch
+  static constexpr int AREA = 2 * TILE + 2 * MB, HAREA = HZ;
   static_assert(NP <= 2 * kWave && Tab::WORDS % 4 == 0 && RF4 * LR == kWave && CPW * D1 == ROW, "layout");
-  static constexpr int LDS_FLOATS = Tab::WORDS + NW * AREA;
+  static constexpr int LDS_FLOATS = Tab::WORDS + NW * AREA + NW * HAREA;
   // first H-table row of round r
   static constexpr int hrow(int r) {
     int o = 0;
@@ -814,6 +832,56 @@ __device__ __forceinline__ void store_tile_f4(__amdgpu_buffer_rsrc_t r, uint32_t
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, int(off), 0, kNonTemporal);
 }
 
+// Counters of the handover between a streaming wave and its helper (LDS).
+struct Handover {
+  int m_ready, m_taken, g_written, g_taken;
+};
+constexpr int kSpinLimit = 1 << 24;  // polls before a wait gives up (about a second)
+
+// Waits until *c >= v (acquire); false if the workgroup has stopped or the wait
+// ran out, in which case the workgroup is stopped.
+__device__ __forceinline__ bool wait_for(int *c, int v, int *stop) {
+  for (int n = 0; n < kSpinLimit; ++n) {
+    if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) return true;
+    if (__hip_atomic_load(stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) return false;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  __hip_atomic_store(stop, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  return false;
+}
+__device__ __forceinline__ void post(int *c, int v) {
+  __hip_atomic_store(c, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// The pair sequence of one streaming wave (and of its helper): pairs fq,
+// fq + total, ... below `pairs`; next() moves to the next pair with edges and
+// calls on_empty(n, u0) for each pair it skips.  Everything about it is
+// wave-uniform; saying so keeps the tile addresses a scalar base plus 32-bit
+// lane offsets.
+template <int GROUPS, int CPW>
+struct PairWalk {
+  int64_t fq, total, pairs, n = 0, eb = 0, e1 = 0;
+  int u0 = 0;
+  static __device__ __forceinline__ int64_t uniform(int64_t v) {
+    const uint64_t u = uint64_t(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u)), hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+    return int64_t((uint64_t(hi) << 32) | lo);
+  }
+  template <class F>
+  __device__ __forceinline__ bool next(const int64_t *__restrict__ row_ptr, F &&on_empty) {
+    while (fq < pairs) {
+      n = fq / GROUPS;
+      u0 = int(fq % GROUPS) * CPW;
+      eb = uniform(row_ptr[n]);
+      e1 = uniform(row_ptr[n + 1]);
+      fq += total;
+      if (e1 > eb) return true;
+      on_empty(n, u0);
+    }
+    return false;
+  }
+};
+
 template <bool FULL, int U, bool WG>
 __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     int64_t N, const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
@@ -825,87 +893,248 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
   constexpr int RF4 = Sh::RF4, LR = Sh::LR, LJ = Sh::LJ, NW = Sh::NW, DEPTH = Sh::DEPTH, GROUPS = U / CPW;
   static_assert(U % CPW == 0, "whole pairs");
   __shared__ float4 smem4[Sh::LDS_FLOATS / 4];
+  __shared__ Handover hand[Sh::NW];
+  __shared__ int stop;
   float *lds = reinterpret_cast<float *>(smem4);
   const uint32_t *tab = reinterpret_cast<const uint32_t *>(lds);
   const uint16_t *tab16 = reinterpret_cast<const uint16_t *>(lds);
   const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave), lane = int(threadIdx.x) % kWave;
-  float *xs = lds + Tab::WORDS + wave * Sh::AREA, *gs = xs + Sh::TILE;
-  float *Gl = xs, *Hz = xs + Sh::GL;  // between tiles
+  const int w = wave % NW;  // the streaming wave of this pair of waves
+  float *xs = lds + Tab::WORDS + w * Sh::AREA, *gs = xs + Sh::TILE;
+  float *mbuf = gs + Sh::TILE, *gbuf = mbuf + Sh::MB;
+  Handover &hv = hand[w];
   {
     const uint4 *src = reinterpret_cast<const uint4 *>(Tab::words());
     for (int i = int(threadIdx.x); i < Tab::WORDS / 4; i += Sh::THREADS) reinterpret_cast<uint4 *>(lds)[i] = src[i];
+    if (threadIdx.x < NW) hand[threadIdx.x] = Handover{-1, -1, -1, -1};
+    if (threadIdx.x == 0) stop = 0;
   }
-  lds_sync<NW>();  // the tables are in LDS (the only barrier of the workgroup)
-  const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x), *g4 = reinterpret_cast<const f32x4 *>(g);
-  f32x4 *gx4 = reinterpret_cast<f32x4 *>(grad_x);
+  lds_sync<2 * NW>();  // tables and counters are set (the only barrier of the workgroup)
   const int64_t total = int64_t(gridDim.x) * NW, pairs = N * GROUPS;
   constexpr uint32_t EDGE_BYTES = U * D1 * 4;  // between consecutive edges in HBM
-  // A lane's offsets within a tile: load lane l moves rows l / RF4 + LR j at
-  // 16-byte column l % RF4; MFMA lane l = 16 h + c.  They are recomputed from
-  // an opaque copy of the lane index where used: held through the loop (they
-  // do not change) they take registers the tiles in flight need.
+  // A lane's offsets within a tile and table offsets are recomputed from
+  // opaque values where used: held through the loop (they do not change) they
+  // take registers the tiles in flight need.
   auto opaque_lane = [&]() {
     int l = lane;
     __asm__ volatile("" : "+v"(l));
     return l;
   };
-  // The tables never change either, so every lookup would be hoisted out of the
-  // pair loop and held; an opaque zero added to the table offsets keeps each
-  // lookup where it is used.
   auto opaque_zero = []() {
     int z = 0;
     __asm__ volatile("" : "+s"(z));
     return z;
   };
+  PairWalk<GROUPS, CPW> walk{int64_t(blockIdx.x) * NW + w, total, pairs};
 
-  // ---- the fetch cursor: the next tile to load (pair fq, edges [feb, feb + 16)).
-  // Everything about it is wave-uniform; saying so keeps the tile addresses a
-  // scalar base plus 32-bit lane offsets.
-  auto uniform = [](int64_t v) {
-    const uint64_t u = uint64_t(v);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u)), hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
-    return int64_t((uint64_t(hi) << 32) | lo);
-  };
-  int64_t fq = int64_t(blockIdx.x) * NW + wave, fn = 0, feb = 0, fe1 = 0;
-  int fu0 = 0;
-  bool fvalid = false, ffirst = false;
-  // pairs of centers without edges have zero sums: written here, no tiles
-  auto seek = [&]() {
-    fvalid = false;
-    while (fq < pairs) {
-      fn = fq / GROUPS;
-      fu0 = int(fq % GROUPS) * CPW;
-      feb = uniform(row_ptr[fn]);
-      fe1 = uniform(row_ptr[fn + 1]);
-      if (fe1 > feb) {
-        fvalid = ffirst = true;
-        return;
+  if (wave >= NW) {
+    // ------------------------------------------------------------ helper wave
+    __builtin_amdgcn_s_setprio(2);
+    float *Hz = lds + Tab::WORDS + NW * Sh::AREA + w * Sh::HAREA;
+    // path weights and env rows of a pair (lanes 0..67 and 0..15), in three
+    // sets: the pair whose M is built (pw0, pw1, pev), the pair whose G is
+    // contracted (qw0, qw1, qev) and the next pair, loaded early (nw0, nw1, nev)
+    float pw0[CPW], pw1[CPW], pev[CPW], qw0[CPW], qw1[CPW], qev[CPW], nw0[CPW], nw1[CPW], nev[CPW];
+    auto load_params = [&](int64_t n, int u0) {
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw) {
+        const int u = u0 + cw;
+        nw0[cw] = lane < NP ? path_w[lane * U + u] : 0.0f;
+        nw1[cw] = lane + kWave < NP ? path_w[(lane + kWave) * U + u] : 0.0f;
+        nev[cw] = lane < D2 ? env[(n * U + u) * D2 + lane] : 0.0f;
       }
-      if (lane < CPW * D2) grad_env[(fn * U + fu0) * D2 + lane] = 0.0f;
-      if constexpr (WG) {
-        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(fn * U + fu0) * NP + i] = 0.0f;
-      }
-      fq += total;
+    };
+    auto wp = [&](int cw, int p) {
+      const float a = __shfl(pw0[cw], p & 63), b = __shfl(pw1[cw], p & 63);
+      return p < kWave ? a : b;
+    };
+    auto wq = [&](int cw, int p) {
+      const float a = __shfl(qw0[cw], p & 63), b = __shfl(qw1[cw], p & 63);
+      return p < kWave ? a : b;
+    };
+    // the lane's M terms 0 and 1 of every slot in registers (coefficients, and
+    // Z indices 10 bits each, three to a word); a third term is read from LDS
+    static_assert(Tab::NZ + 2 <= 1024 && S * kWave <= 1024, "10-bit table indices");
+    constexpr int MTS = (Tab::MT < 2 ? Tab::MT : 2) * S;
+    float mc[MTS];
+    uint32_t mi[(MTS + 2) / 3];  // three 10-bit indices per word
+#pragma unroll
+    for (int q = 0; q < MTS; ++q) mc[q] = __uint_as_float(tab[Tab::OFF_MC + q * kWave + lane]);
+#pragma unroll
+    for (int q = 0; q < (MTS + 2) / 3; ++q) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int b = 0; b < 3; ++b)
+        if (3 * q + b < MTS) v |= uint32_t(tab16[2 * Tab::OFF_MI + (3 * q + b) * kWave + lane]) << (10 * b);
+      mi[q] = v;
     }
-  };
+    // the lane's H term indices (10 bits, three per word)
+    uint32_t hi[(Tab::TH + 2) / 3];
+#pragma unroll
+    for (int q = 0; q < (Tab::TH + 2) / 3; ++q) {
+      uint32_t v = 0;
+#pragma unroll
+      for (int b = 0; b < 3; ++b)
+        if (3 * q + b < Tab::TH) v |= uint32_t(tab16[2 * Tab::OFF_HI + (3 * q + b) * kWave + lane]) << (10 * b);
+      hi[q] = v;
+    }
+    // M of the pair into the M buffer, lane layout [cw][slot][64]
+    auto build_m = [&]() {
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw) {
+        lds_sync<1>();  // Hz is free
+#pragma unroll
+        for (int r = 0; r < Tab::RZ; ++r) {
+          const uint32_t pj = tab[Tab::OFF_ZP + kWave * r + lane];
+          Hz[kWave * r + lane] = wp(cw, int(pj & 0xffffu)) * __shfl(pev[cw], int(pj >> 16));
+        }
+        lds_sync<1>();
+#pragma unroll
+        for (int sl = 0; sl < S; ++sl) {
+          float a = 0.0f;
+#pragma unroll
+          for (int t = 0; t < Tab::MT; ++t) {
+            const int q = t * S + sl;
+            if (q < MTS) {
+              a = __builtin_fmaf(mc[q], Hz[(mi[q / 3] >> (10 * (q % 3))) & 0x3ffu], a);
+            } else {
+              const int row = opaque_zero() + q * kWave + lane;
+              a = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_MC + row]), Hz[tab16[2 * Tab::OFF_MI + row]], a);
+            }
+          }
+          mbuf[(cw * S + sl) * kWave + lane] = a;
+        }
+      }
+    };
+    // contraction of the pair's G (in the G buffer): H, grad_env, path-weight rows
+    auto contract_g = [&](int64_t n, int u0) {
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw) {
+        const int z0 = opaque_zero();
+        const int u = u0 + cw;
+        const float *Gl = gbuf + cw * S * kWave;
+        lds_sync<1>();  // Hz is free
+        if (lane == 0) Hz[Tab::NZ] = 0.0f;
+        static_for<0, Tab::RH>([&](auto rc) {
+          constexpr int r = decltype(rc)::value, r0 = Sh::hrow(r);
+          float hv = 0.0f;
+#pragma unroll
+          for (int t = 0; t < Tab::HT[r]; ++t) {
+            const int row = z0 + (r0 + t) * kWave + lane;
+            const int q = r0 + t;
+            hv = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_HC + row]), Gl[(hi[q / 3] >> (10 * (q % 3))) & 0x3ffu], hv);
+          }
+          Hz[tab16[2 * Tab::OFF_HT + z0 + r * kWave + lane]] = hv;
+          __asm__ volatile("" : : : "memory");
+        });
+        lds_sync<1>();
+        float ge = 0.0f;
+#pragma unroll
+        for (int t = 0; t < Tab::TGE; ++t) {
+          const uint32_t wd = tab[Tab::OFF_GE + z0 + t * kWave + lane];
+          ge = __builtin_fmaf(Hz[wd & 0xffffu], wq(cw, int(wd >> 16)), ge);
+        }
+        ge += __shfl_xor(ge, 1);
+        ge += __shfl_xor(ge, 2);
+        if ((lane & 3) == 0) grad_env[(n * U + u) * D2 + lane / 4] = ge;
+        if constexpr (WG) {
+#pragma unroll
+          for (int r = 0; r < Tab::RPW; ++r) {
+            const int p = kWave * r + lane;
+            const uint32_t wd = tab[Tab::OFF_PW + z0 + p];
+            const int off = int(wd & 0xffffu), len = int(wd >> 16);
+            // the shuffle reads env from lanes 0..15, so every lane takes it:
+            // the loop runs to the longest path's length, shorter ones add zeros
+            float a = 0.0f;
+            for (int k = 0; k < Tab::PWMAX; ++k) {
+              const bool in = k < len;
+              const uint32_t zp = tab[Tab::OFF_ZP + z0 + (in ? off + k : 0)];
+              const float e = __shfl(qev[cw], int(zp >> 16));
+              a = __builtin_fmaf(in ? Hz[off + k] : 0.0f, e, a);
+            }
+            if (p < NP) pw_part[(n * U + u) * NP + p] = a;  // channel-major row: one contiguous store
+          }
+        }
+      }
+    };
+    // pairs without edges have zero sums: written here, no tiles
+    auto on_empty = [&](int64_t n, int u0) {
+      if (lane < CPW * D2) grad_env[(n * U + u0) * D2 + lane] = 0.0f;
+      if constexpr (WG) {
+        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(n * U + u0) * NP + i] = 0.0f;
+      }
+    };
+    int64_t prev_n = 0;
+    int prev_u0 = 0;
+    int k = 0;
+    auto rotate = [&]() {
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw) {
+        qw0[cw] = pw0[cw];
+        qw1[cw] = pw1[cw];
+        qev[cw] = pev[cw];
+        pw0[cw] = nw0[cw];
+        pw1[cw] = nw1[cw];
+        pev[cw] = nev[cw];
+      }
+    };
+    bool have = walk.next(row_ptr, on_empty);
+    if (have) load_params(walk.n, walk.u0);
+    rotate();
+    while (have) {
+      const int64_t cn = walk.n;
+      const int cu0 = walk.u0;
+      if (!wait_for(&hv.m_taken, k - 1, &stop)) return;  // the wave has taken the previous M
+      build_m();
+      post(&hv.m_ready, k);
+      have = walk.next(row_ptr, on_empty);
+      if (have) load_params(walk.n, walk.u0);
+      if (k > 0) {
+        if (!wait_for(&hv.g_written, k - 1, &stop)) return;
+        contract_g(prev_n, prev_u0);
+        post(&hv.g_taken, k - 1);
+      }
+      rotate();
+      prev_n = cn;
+      prev_u0 = cu0;
+      ++k;
+    }
+    if (k > 0 && wait_for(&hv.g_written, k - 1, &stop)) {
+      contract_g(prev_n, prev_u0);
+      post(&hv.g_taken, k - 1);
+    }
+    return;
+  }
+
+  // -------------------------------------------------------- streaming wave
+  const f32x4 *x4 = reinterpret_cast<const f32x4 *>(x), *g4 = reinterpret_cast<const f32x4 *>(g);
+  f32x4 *gx4 = reinterpret_cast<f32x4 *>(grad_x);
+  auto no_op = [](int64_t, int) {};
+  // the fetch cursor: the next tile to load (edges [feb, feb + 16) of the walk's pair)
+  bool fvalid = walk.next(row_ptr, no_op), ffirst = true;
+  int64_t feb = walk.eb;
   // the ring of tiles in flight: slot d holds a tile and its identity
   f32x4 vx[DEPTH][LJ], vg[DEPTH][LJ];
   int64_t s_n[DEPTH], s_eb[DEPTH], s_e1[DEPTH];
   int s_u0[DEPTH];
   bool s_valid[DEPTH], s_first[DEPTH];
+  // Every tile, valid or not, issues the same memory instructions (an empty
+  // tile's descriptors have no range: its loads read zeros and its stores are
+  // dropped), so that on every path the same loads are in flight and each
+  // wait for a tile's data waits for that tile's loads only.
   auto fetch = [&](int d) {
     s_valid[d] = fvalid;
-    if (!fvalid) return;
-    s_n[d] = fn;
-    s_u0[d] = fu0;
+    s_n[d] = walk.n;
+    s_u0[d] = walk.u0;
     s_eb[d] = feb;
-    s_e1[d] = fe1;
+    s_e1[d] = walk.e1;
     s_first[d] = ffirst;
     ffirst = false;
     // buffer loads from the tile's first row: rows past the segment lie past
     // the descriptor's range and read as zero
-    const int64_t base = (feb * U + fu0) * (D1 / 4);
-    const uint32_t bytes = uint32_t(fe1 - feb < kMfmaEdges ? fe1 - feb : kMfmaEdges) * EDGE_BYTES;
+    const int64_t base = (feb * U + walk.u0) * (D1 / 4);
+    const uint32_t bytes =
+        fvalid ? uint32_t(walk.e1 - feb < kMfmaEdges ? walk.e1 - feb : kMfmaEdges) * EDGE_BYTES : 0u;
     const auto rx = tile_rsrc(x4 + base, bytes), rg = tile_rsrc(g4 + base, bytes);
     const int ln = opaque_lane();
     const uint32_t voff = uint32_t(ln / RF4) * EDGE_BYTES + uint32_t(ln % RF4) * 16u;
@@ -914,131 +1143,50 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
       vx[d][j] = load_tile_f4(rx, voff + uint32_t(LR * j) * EDGE_BYTES);
       vg[d][j] = load_tile_f4(rg, voff + uint32_t(LR * j) * EDGE_BYTES);
     }
-    feb += kMfmaEdges;
-    if (feb >= fe1) {
-      fq += total;
-      seek();
+    if (fvalid) {
+      feb += kMfmaEdges;
+      if (feb >= walk.e1) {
+        fvalid = walk.next(row_ptr, no_op);
+        ffirst = true;
+        feb = walk.eb;
+      }
     }
   };
 
-  // the pair whose tiles are being multiplied: its identity, M and G
-  int64_t p_n = 0;
-  int p_u0 = 0;
-  bool have_pair = false;
-  // the pair's path weights and env rows, loaded where they are used (the
-  // prologue and the contraction) rather than held through the tile loop
-  float pw0[CPW], pw1[CPW], pev[CPW];
-  auto load_params = [&]() {
-#pragma unroll
-    for (int cw = 0; cw < CPW; ++cw) {
-      const int u = p_u0 + cw;
-      pw0[cw] = lane < NP ? path_w[lane * U + u] : 0.0f;
-      pw1[cw] = lane + kWave < NP ? path_w[(lane + kWave) * U + u] : 0.0f;
-      pev[cw] = lane < D2 ? env[(p_n * U + u) * D2 + lane] : 0.0f;
-    }
-  };
+  // the pair whose tiles are being multiplied: its M and G
   float m[CPW][S];
   f32x4 Gacc[CPW][NT * NT];
-  // W(p) and env[j] of channel cw of the current pair, from the lanes that hold them
-  auto wp = [&](int cw, int p) {
-    const float a = __shfl(pw0[cw], p & 63), b = __shfl(pw1[cw], p & 63);
-    return p < kWave ? a : b;
-  };
-  auto ej = [&](int cw, int j) { return __shfl(pev[cw], j); };
-
-  // contraction of G for the current pair: spill, H, grad_env, path-weight row
-  auto finish_pair = [&]() {
-    load_params();
+  int k = -1;  // index of that pair in the wave's sequence
+  // G of pair k to the helper (after it has contracted pair k - 1's)
+  auto hand_g = [&]() {
+    wait_for(&hv.g_taken, k - 1, &stop);
 #pragma unroll
-    for (int cw = 0; cw < CPW; ++cw) {
-      const int z0 = opaque_zero();
-      const int u = p_u0 + cw;
-      lds_sync<1>();  // the LDS area (or the previous channel's H) is free
+    for (int cw = 0; cw < CPW; ++cw)
 #pragma unroll
       for (int t = 0; t < NT * NT; ++t)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) Gl[(t * 4 + r) * kWave + lane] = Gacc[cw][t][r];
-      if (lane == 0) Hz[Tab::NZ] = 0.0f;
-      lds_sync<1>();
-      static_for<0, Tab::RH>([&](auto rc) {
-        constexpr int r = decltype(rc)::value, r0 = Sh::hrow(r);
-        float hv = 0.0f;
-#pragma unroll
-        for (int t = 0; t < Tab::HT[r]; ++t) {
-          const int row = z0 + (r0 + t) * kWave + lane;
-          hv = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_HC + row]), Gl[tab16[2 * Tab::OFF_HI + row]], hv);
-        }
-        Hz[tab16[2 * Tab::OFF_HT + z0 + r * kWave + lane]] = hv;
-        __asm__ volatile("" : : : "memory");
-      });
-      lds_sync<1>();
-      float ge = 0.0f;
-#pragma unroll
-      for (int t = 0; t < Tab::TGE; ++t) {
-        const uint32_t wd = tab[Tab::OFF_GE + z0 + t * kWave + lane];
-        ge = __builtin_fmaf(Hz[wd & 0xffffu], wp(cw, int(wd >> 16)), ge);
-      }
-      ge += __shfl_xor(ge, 1);
-      ge += __shfl_xor(ge, 2);
-      if ((lane & 3) == 0) grad_env[(p_n * U + u) * D2 + lane / 4] = ge;
-      if constexpr (WG) {
-#pragma unroll
-        for (int r = 0; r < Tab::RPW; ++r) {
-          const int p = kWave * r + lane;
-          const uint32_t wd = tab[Tab::OFF_PW + z0 + p];
-          const int off = int(wd & 0xffffu), len = int(wd >> 16);
-          // the shuffle reads env from lanes 0..15, so every lane takes it:
-          // the loop runs to the longest path's length, shorter ones add zeros
-          float a = 0.0f;
-          for (int k = 0; k < Tab::PWMAX; ++k) {
-            const bool in = k < len;
-            const uint32_t zp = tab[Tab::OFF_ZP + z0 + (in ? off + k : 0)];
-            const float e = __shfl(pev[cw], int(zp >> 16));
-            a = __builtin_fmaf(in ? Hz[off + k] : 0.0f, e, a);
-          }
-          if (p < NP) pw_part[(p_n * U + u) * NP + p] = a;  // channel-major row: one contiguous store
-        }
-      }
-    }
-  };
-  // the new pair: parameters, Z[q] = W(p) env[j] and M's cells, channel by channel
-  auto start_pair = [&](int64_t n, int u0) {
-    p_n = n;
-    p_u0 = u0;
-    have_pair = true;
-    load_params();
-#pragma unroll
-    for (int cw = 0; cw < CPW; ++cw) {
-      const int z0 = opaque_zero();
-      lds_sync<1>();  // Hz is free
-#pragma unroll
-      for (int r = 0; r < Tab::RZ; ++r) {
-        const uint32_t pj = tab[Tab::OFF_ZP + z0 + kWave * r + lane];
-        Hz[kWave * r + lane] = wp(cw, int(pj & 0xffffu)) * ej(cw, int(pj >> 16));
-      }
-      lds_sync<1>();
-#pragma unroll
-      for (int sl = 0; sl < S; ++sl) {
-        float a = 0.0f;
-#pragma unroll
-        for (int t = 0; t < Tab::MT; ++t) {
-          const int row = z0 + (t * S + sl) * kWave + lane;
-          a = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_MC + row]), Hz[tab16[2 * Tab::OFF_MI + row]], a);
-        }
-        m[cw][sl] = a;
-      }
-#pragma unroll
-      for (int t = 0; t < NT * NT; ++t) Gacc[cw][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    }
-    lds_sync<1>();  // Hz is read before the tile overwrites it
+        for (int r = 0; r < 4; ++r) gbuf[((cw * NT * NT + t) * 4 + r) * kWave + lane] = Gacc[cw][t][r];
+    post(&hv.g_written, k);
   };
   // one tile, from ring slot d: grad_x rows out, G accumulated
   auto tile = [&](int d) {
-    if (s_first[d]) {
-      if (have_pair) finish_pair();
-      start_pair(s_n[d], s_u0[d]);
+    if (s_valid[d] && s_first[d]) {
+      if (k >= 0) hand_g();
+      ++k;
+      wait_for(&hv.m_ready, k, &stop);
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw) {
+#pragma unroll
+        for (int sl = 0; sl < S; ++sl) m[cw][sl] = mbuf[(cw * S + sl) * kWave + lane];
+#pragma unroll
+        for (int t = 0; t < NT * NT; ++t) Gacc[cw][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+      post(&hv.m_taken, k);
     }
+    // the slot's identity, read before fetch(d) below refills the slot
     const int64_t teb = s_eb[d], te1 = s_e1[d];
+    const int tu0 = s_u0[d];
+    const bool tvalid = s_valid[d];
     int ln = opaque_lane();
     {
       const int le = ln / RF4, lc = ln % RF4;
@@ -1053,21 +1201,6 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     const int h = ln / 16, c = ln % 16;
 #pragma unroll
     for (int cw = 0; cw < CPW; ++cw) {
-      // grad_x[e][i] = sum_k g[e][k] M[k][i]: A = the g rows of the 16 edges
-      f32x4 gA[NT];
-#pragma unroll
-      for (int tk = 0; tk < NT; ++tk)
-        gA[tk] = *reinterpret_cast<const f32x4 *>(gs + swz32(c, D1 * cw + 16 * tk + 4 * h));
-      f32x4 D[NT];
-#pragma unroll
-      for (int ti = 0; ti < NT; ++ti) {
-        D[ti] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int tk = 0; tk < NT; ++tk)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            D[ti] = __builtin_amdgcn_mfma_f32_16x16x4f32(gA[tk][r], m[cw][(tk * NT + ti) * 4 + r], D[ti], 0, 0, 0);
-      }
       // G[k][i] += sum_e g[e][k] x[e][i], four edges (4 st + h) per step
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
@@ -1085,6 +1218,22 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
             Gacc[cw][tk * NT + ti] =
                 __builtin_amdgcn_mfma_f32_16x16x4f32(gG[tk], xG[ti], Gacc[cw][tk * NT + ti], 0, 0, 0);
       }
+      // grad_x[e][i] = sum_k g[e][k] M[k][i]: A = the g rows of the 16 edges;
+      // formed after G, so that its accumulators are not live beside G's operands
+      f32x4 gA[NT];
+#pragma unroll
+      for (int tk = 0; tk < NT; ++tk)
+        gA[tk] = *reinterpret_cast<const f32x4 *>(gs + swz32(c, D1 * cw + 16 * tk + 4 * h));
+      f32x4 D[NT];
+#pragma unroll
+      for (int ti = 0; ti < NT; ++ti) {
+        D[ti] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int tk = 0; tk < NT; ++tk)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            D[ti] = __builtin_amdgcn_mfma_f32_16x16x4f32(gA[tk][r], m[cw][(tk * NT + ti) * 4 + r], D[ti], 0, 0, 0);
+      }
       // this channel's x columns are no longer needed: its grad_x rows go there
       lds_sync<1>();
 #pragma unroll
@@ -1095,8 +1244,8 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     lds_sync<1>();
     {
       // rows past the segment lie past the descriptor's range: not written
-      const uint32_t bytes = uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES;
-      const auto ro = tile_rsrc(gx4 + (teb * U + p_u0) * (D1 / 4), bytes);
+      const uint32_t bytes = tvalid ? uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES : 0u;
+      const auto ro = tile_rsrc(gx4 + (teb * U + tu0) * (D1 / 4), bytes);
       ln = opaque_lane();
       const int se = ln / RF4, sc = ln % RF4;
       const uint32_t voff = uint32_t(se) * EDGE_BYTES + uint32_t(sc) * 16u;
@@ -1108,22 +1257,19 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     lds_sync<1>();  // the LDS area is free again
   };
 
-  seek();
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) fetch(d);
-  bool more = true;
-  while (more) {
+  // rounds of DEPTH tiles while any is valid; the empty ones at the end of the
+  // sequence run as zero tiles (their products add zeros, their stores drop)
+  for (;;) {
+    bool any = false;
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      if (more) {
-        if (s_valid[d])
-          tile(d);
-        else
-          more = false;
-      }
-    }
+    for (int d = 0; d < DEPTH; ++d) any |= s_valid[d];
+    if (!any) break;
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) tile(d);
   }
-  if (have_pair) finish_pair();
+  if (k >= 0) hand_g();
 }
 
 // ------------------------------------------------------ spherical harmonics

@@ -389,9 +389,12 @@ def test_sh_headline_vectors_sampled(at):
 # ------------------------------------------ training backward (path weights)
 
 def _train(at, plan, rp, x, env, pw, g, w, y):
+    """The training backward into outputs filled with NaN, so that an element the
+    kernels leave unwritten fails every comparison."""
     n = rp.numel() - 1
     ws = torch.empty(at.allegro_tp_backward_workspace(plan, n), dtype=torch.uint8, device=DEV)
-    res = at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, workspace=ws)
+    outs = tuple(torch.full_like(a, float("nan")) for a in (x, env, w, y, pw))
+    res = at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, outs=outs, workspace=ws)
     torch.cuda.synchronize()
     return res, ws
 
@@ -477,7 +480,11 @@ def test_train_backward_full_size(at, name, n_samples=16):
     pw = workloads.path_weights(cfg)
     rp, yd, pwd = _t(graph.row_ptr), _t(graph.Y), _t(pw)
     env = at.allegro_env_embed(plan, rp, w, yd)
-    (gx, _, _, _, gpw), ws = _train(at, plan, rp, x, env, pwd, g, w, yd)
+    (gx, genv, gw, gy, gpw), ws = _train(at, plan, rp, x, env, pwd, g, w, yd)
+    # every element written (the outputs start as NaN)
+    for name_, a in (("grad_x", gx), ("grad_env", genv), ("grad_w", gw), ("grad_Y", gy), ("grad_path_w", gpw)):
+        assert not bool(torch.isnan(a).any()), f"{name_} has unwritten elements"
+    del genv, gw, gy
     n, cols = graph.n_atoms, plan.n_paths * cfg.U
     rows = ws[: n * cols * 4].view(torch.float32)
     # a center's row is path-major [P][U], or channel-major [U][P] at lmax 3
