@@ -739,13 +739,18 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 // (M is the forward's per-center matrix), and the segment sums follow from G:
 //   grad_env[j] = sum_{(k,i)} sum_p W(p) C_pijk G[k][i],
 //   grad_W[p]  += sum_{(k,i)} sum_j C_pijk env[j] G[k][i]   (training only).
-// Both products run on v_mfma_f32_16x16x4f32: for grad_x the 16 edges of a
-// tile are the rows and k the reduction (d1 / 4 steps per 16 columns of i),
-// for G the edges are the reduction (4 per step) and (k, i) the 16 x 16 output
-// tiles.  Lane l = 16 h + c holds, in slot s = (tk * NT + ti) * 4 + r, the cell
-// (k, i) = (16 tk + 4 h + r, 16 ti + c) of M (B operand of grad_x) and of G
-// (accumulator); the generated tables (TPMfmaTab) build M's cells and contract
-// G's cells lane by lane from the sparse coupling table.
+// Both products run on v_mfma_f32_16x16x4f32.  grad_x is formed transposed,
+// grad_x^T = M^T g^T: M is the A operand, the 16 edges of a tile are the
+// columns and k the reduction (d1 / 4 steps per 16 rows i), so that each lane
+// ends with four consecutive columns of one edge's grad_x row and stores them
+// as they are.  For G the edges are the reduction (4 per step) and (k, i) the
+// 16 x 16 output tiles.  Lane l = 16 h + c holds, in slot s = (tk * NT + ti) *
+// 4 + r, the cell (k, i) = (16 tk + 4 h + r, 16 ti + c) of M; of G it holds the
+// cell (2 (4 h + r) + tk, 2 c + ti) when d1 = 32 (its operands are read as
+// pairs of adjacent columns) and the same cell as of M otherwise.  The
+// generated tables (TPMfmaTab) build M's cells and contract G's cells lane by
+// lane from the sparse coupling table; M and G cross between the waves in a
+// lane-major spill (MfmaShape::spill), 16 bytes at a time.
 //
 // Work: the pairs (center n, CPW consecutive channels; CPW = 32 / d1, so that a
 // pair's row of one edge is 128 contiguous bytes: one channel with full
@@ -799,6 +804,10 @@ struct MfmaShape {
   static constexpr int AREA = 2 * TILE + 2 * MB, HAREA = HZ;
   static_assert(NP <= 2 * kWave && Tab::WORDS % 4 == 0 && RF4 * LR == kWave && CPW * D1 == ROW, "layout");
   static constexpr int LDS_FLOATS = Tab::WORDS + NW * AREA + NW * HAREA;
+  // float offset of slot group q (slots 4 q .. 4 q + 3) of lane l in a spill of
+  // M or G: lane-major, groups XOR-swizzled by (l / 4) mod (S / 4) so that the
+  // 16-byte accesses of eight consecutive lanes hit distinct banks
+  static __device__ __forceinline__ int spill(int l, int q) { return l * S + 4 * (q ^ ((l >> 2) & (S / 4 - 1))); }
   // first H-table row of round r
   static constexpr int hrow(int r) {
     int o = 0;
@@ -978,7 +987,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
         if (3 * q + b < Tab::TH) v |= uint32_t(tab16[2 * Tab::OFF_HI + (3 * q + b) * kWave + lane]) << (10 * b);
       hi[q] = v;
     }
-    // M of the pair into the M buffer, lane layout [cw][slot][64]
+    // M of the pair into the M buffer (the spill layout, per channel of the pair)
     auto build_m = [&]() {
 #pragma unroll
       for (int cw = 0; cw < CPW; ++cw) {
@@ -990,19 +999,25 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
         }
         lds_sync<1>();
 #pragma unroll
-        for (int sl = 0; sl < S; ++sl) {
-          float a = 0.0f;
+        for (int sg = 0; sg < S / 4; ++sg) {
+          f32x4 a4;
 #pragma unroll
-          for (int t = 0; t < Tab::MT; ++t) {
-            const int q = t * S + sl;
-            if (q < MTS) {
-              a = __builtin_fmaf(mc[q], Hz[(mi[q / 3] >> (10 * (q % 3))) & 0x3ffu], a);
-            } else {
-              const int row = opaque_zero() + q * kWave + lane;
-              a = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_MC + row]), Hz[tab16[2 * Tab::OFF_MI + row]], a);
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const int sl = 4 * sg + r4;
+            float a = 0.0f;
+#pragma unroll
+            for (int t = 0; t < Tab::MT; ++t) {
+              const int q = t * S + sl;
+              if (q < MTS) {
+                a = __builtin_fmaf(mc[q], Hz[(mi[q / 3] >> (10 * (q % 3))) & 0x3ffu], a);
+              } else {
+                const int row = opaque_zero() + q * kWave + lane;
+                a = __builtin_fmaf(__uint_as_float(tab[Tab::OFF_MC + row]), Hz[tab16[2 * Tab::OFF_MI + row]], a);
+              }
             }
+            a4[r4] = a;
           }
-          mbuf[(cw * S + sl) * kWave + lane] = a;
+          *reinterpret_cast<f32x4 *>(mbuf + cw * S * kWave + Sh::spill(opaque_lane(), sg)) = a4;
         }
       }
     };
@@ -1163,9 +1178,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
 #pragma unroll
     for (int cw = 0; cw < CPW; ++cw)
 #pragma unroll
-      for (int t = 0; t < NT * NT; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) gbuf[((cw * NT * NT + t) * 4 + r) * kWave + lane] = Gacc[cw][t][r];
+      for (int t = 0; t < NT * NT; ++t) *reinterpret_cast<f32x4 *>(gbuf + cw * S * kWave + Sh::spill(opaque_lane(), t)) = Gacc[cw][t];
     post(&hv.g_written, k);
   };
   // one tile, from ring slot d: grad_x rows out, G accumulated
@@ -1177,7 +1190,11 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
 #pragma unroll
       for (int cw = 0; cw < CPW; ++cw) {
 #pragma unroll
-        for (int sl = 0; sl < S; ++sl) m[cw][sl] = mbuf[(cw * S + sl) * kWave + lane];
+        for (int sg = 0; sg < S / 4; ++sg) {
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(mbuf + cw * S * kWave + Sh::spill(opaque_lane(), sg));
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) m[cw][4 * sg + r4] = v[r4];
+        }
 #pragma unroll
         for (int t = 0; t < NT * NT; ++t) Gacc[cw][t] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       }
@@ -1199,17 +1216,30 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     fetch(d);  // the slot takes the tile DEPTH ahead
     lds_sync<1>();
     const int h = ln / 16, c = ln % 16;
+    // rows past the segment lie past the descriptor's range: not written
+    const uint32_t obytes = tvalid ? uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES : 0u;
+    const auto ro = tile_rsrc(gx4 + (teb * U + tu0) * (D1 / 4), obytes);
 #pragma unroll
     for (int cw = 0; cw < CPW; ++cw) {
       // G[k][i] += sum_e g[e][k] x[e][i], four edges (4 st + h) per step
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
         float gG[NT], xG[NT];
+        if constexpr (Tab::GPAIR) {
+          // columns 2 c and 2 c + 1 in one read: tile t takes the columns 2 c + t
+          const int o = swz32(4 * st + h, 2 * c);
+          const float2 gv = *reinterpret_cast<const float2 *>(gs + o), xv = *reinterpret_cast<const float2 *>(xs + o);
+          gG[0] = gv.x;
+          gG[1] = gv.y;
+          xG[0] = xv.x;
+          xG[1] = xv.y;
+        } else {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const int o = swz32(4 * st + h, D1 * cw + 16 * t + c);
-          gG[t] = gs[o];
-          xG[t] = xs[o];
+          for (int t = 0; t < NT; ++t) {
+            const int o = swz32(4 * st + h, D1 * cw + 16 * t + c);
+            gG[t] = gs[o];
+            xG[t] = xs[o];
+          }
         }
 #pragma unroll
         for (int tk = 0; tk < NT; ++tk)
@@ -1218,43 +1248,27 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
             Gacc[cw][tk * NT + ti] =
                 __builtin_amdgcn_mfma_f32_16x16x4f32(gG[tk], xG[ti], Gacc[cw][tk * NT + ti], 0, 0, 0);
       }
-      // grad_x[e][i] = sum_k g[e][k] M[k][i]: A = the g rows of the 16 edges;
-      // formed after G, so that its accumulators are not live beside G's operands
+      // grad_x^T[i][e] = sum_k M[k][i] g[e][k], with M as the A operand and the g
+      // rows of the 16 edges as B, so that lane 16 h + c ends with the four
+      // consecutive columns 16 ti + 4 h .. + 3 of edge c's grad_x row, stored as
+      // they are; formed after G, so that its accumulators are not live beside
+      // G's operands
       f32x4 gA[NT];
 #pragma unroll
       for (int tk = 0; tk < NT; ++tk)
         gA[tk] = *reinterpret_cast<const f32x4 *>(gs + swz32(c, D1 * cw + 16 * tk + 4 * h));
-      f32x4 D[NT];
 #pragma unroll
       for (int ti = 0; ti < NT; ++ti) {
-        D[ti] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+        f32x4 D = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int tk = 0; tk < NT; ++tk)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            D[ti] = __builtin_amdgcn_mfma_f32_16x16x4f32(gA[tk][r], m[cw][(tk * NT + ti) * 4 + r], D[ti], 0, 0, 0);
+            D = __builtin_amdgcn_mfma_f32_16x16x4f32(m[cw][(tk * NT + ti) * 4 + r], gA[tk][r], D, 0, 0, 0);
+        store_tile_f4(ro, uint32_t(c) * EDGE_BYTES + uint32_t(D1 * cw + 16 * ti + 4 * h) * 4u, D);
       }
-      // this channel's x columns are no longer needed: its grad_x rows go there
-      lds_sync<1>();
-#pragma unroll
-      for (int ti = 0; ti < NT; ++ti)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) xs[swz32(4 * h + r, D1 * cw + 16 * ti + c)] = D[ti][r];
     }
-    lds_sync<1>();
-    {
-      // rows past the segment lie past the descriptor's range: not written
-      const uint32_t bytes = tvalid ? uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES : 0u;
-      const auto ro = tile_rsrc(gx4 + (teb * U + tu0) * (D1 / 4), bytes);
-      ln = opaque_lane();
-      const int se = ln / RF4, sc = ln % RF4;
-      const uint32_t voff = uint32_t(se) * EDGE_BYTES + uint32_t(sc) * 16u;
-#pragma unroll
-      for (int j = 0; j < LJ; ++j)
-        store_tile_f4(ro, voff + uint32_t(LR * j) * EDGE_BYTES,
-                      *reinterpret_cast<const f32x4 *>(xs + swz32(se + LR * j, 4 * sc)));
-    }
-    lds_sync<1>();  // the LDS area is free again
+    lds_sync<1>();  // the tile's LDS reads are done: the area is free again
   };
 
 #pragma unroll

@@ -297,8 +297,10 @@ void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name) {
 // which run on v_mfma_f32_16x16x4f32.  In its operand and result layout lane
 // l = 16 h + c of a wave holds, for slot s = (tk * NT + ti) * 4 + r, the cell
 //   (k, i) = (16 tk + 4 h + r, 16 ti + c)
-// of M (as the B operand of grad_x, K = k) and of G (as the accumulator), so one
-// assignment of cells to (lane, slot) serves both.  The tables let every lane
+// of M (as the A operand of grad_x^T = M^T g^T, K = k), and the same cell of G
+// (the accumulator) except with d1 = 32, where G's operands are read as pairs
+// of adjacent columns and the lane holds G's cell (2 (4 h + r) + tk, 2 c + ti).
+// M and G cross between waves as a lane-major spill (spill_pos).  The tables let every lane
 // form its own cells of M and contract its cells of G without any lane-uniform
 // code:
 //   Z[q] = W(p) env[j] for the q-th distinct (p, j) of the coupling table
@@ -307,7 +309,7 @@ void emit_matrix(FILE *f, const allegro::TPTable &t, int nw, const char *name) {
 //          padded with zero coefficients);
 //   H[q] = sum over the cells (k, i) of path p, env component j of C_pijk G[k][i]
 //          (H rounds: lane -> target q, HT[round] terms of (coefficient, index
-//          of the cell in the wave's G spill [slot][64]));
+//          of the cell in the G spill));
 //   grad_env[j] = sum_q W(p(q)) H[q] over the q with j(q) = j: lane 4 j + quarter
 //          sums every fourth such q (words q | p << 16, padded with q = NZ,
 //          where H[NZ] = 0), then the four quarters are added by lane shuffles;
@@ -331,9 +333,24 @@ void emit_mfma_tables(FILE *f, const allegro::TPTable &t) {
     const int h = lane / 16, c = lane % 16, r = slot % 4, tk = (slot / 4) / nt, ti = (slot / 4) % nt;
     return std::make_pair(16 * tk + 4 * h + r, 16 * ti + c);  // (k, i)
   };
-  auto gidx_of = [&](int k, int i) {  // position of cell (k, i) in the [slot][64] spill
+  // With d1 = 32 the kernel reads the G products' operands as pairs of adjacent
+  // columns, so product tile t (of the two per operand) takes the columns 2 c + t
+  // and G's cell (k, i) sits in tile (k % 2, i % 2) at row k / 2, column i / 2.
+  // The spill of a lane's cells is lane-major: the S slots of lane l start at
+  // l S, in groups of four (one 16-byte access) whose order is XOR-swizzled by
+  // (l / 4) mod (S / 4), so that eight lanes' 16-byte accesses hit distinct banks.
+  const bool gpair = d1 == 32;
+  auto spill_pos = [&](int lane, int slot) {
+    const int q = slot / 4, r = slot % 4;
+    return lane * S + 4 * (q ^ ((lane / 4) & (S / 4 - 1))) + r;
+  };
+  auto gidx_of = [&](int k, int i) {  // position of cell (k, i) in the spill
+    if (gpair) {
+      const int tk = k % 2, m = k / 2, h = m / 4, r = m % 4, ti = i % 2, c = i / 2;
+      return spill_pos(16 * h + c, (tk * nt + ti) * 4 + r);
+    }
     const int tk = k / 16, h = (k % 16) / 4, r = k % 4, ti = i / 16, c = i % 16;
-    return ((tk * nt + ti) * 4 + r) * 64 + 16 * h + c;
+    return spill_pos(16 * h + c, (tk * nt + ti) * 4 + r);
   };
   // M terms per cell
   std::map<std::pair<int, int>, std::vector<std::pair<double, int>>> mterms;
@@ -442,6 +459,7 @@ void emit_mfma_tables(FILE *f, const allegro::TPTable &t) {
   std::fprintf(f, "template <> struct TPMfmaTab<%d, %s> {\n", t.lmax, full);
   std::fprintf(f, "  static constexpr int D1 = %d, NT = %d, S = %d, NP = %d, NZ = %d, RZ = %d, MT = %d, RH = %d, TH = %d, "
                   "TGE = %d, RPW = %d, PWMAX = %d;\n", d1, nt, S, np, nz, rz, mt, rh, th, tge, rpw, pwmax);
+  std::fprintf(f, "  static constexpr bool GPAIR = %s;  // G operands read as column pairs\n", gpair ? "true" : "false");
   std::fprintf(f, "  static constexpr int HT[%d] = {", rh);
   for (int r = 0; r < rh; ++r) std::fprintf(f, "%s%d", r ? ", " : "", ht[r]);
   std::fprintf(f, "};\n");
