@@ -1219,6 +1219,8 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     // rows past the segment lie past the descriptor's range: not written
     const uint32_t obytes = tvalid ? uint32_t(te1 - teb < kMfmaEdges ? te1 - teb : kMfmaEdges) * EDGE_BYTES : 0u;
     const auto ro = tile_rsrc(gx4 + (teb * U + tu0) * (D1 / 4), obytes);
+    static_assert(CPW * NT == 2, "a tile's row is two 16-column blocks");
+    f32x4 Dout[2];
 #pragma unroll
     for (int cw = 0; cw < CPW; ++cw) {
       // G[k][i] += sum_e g[e][k] x[e][i], four edges (4 st + h) per step
@@ -1250,9 +1252,8 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
       }
       // grad_x^T[i][e] = sum_k M[k][i] g[e][k], with M as the A operand and the g
       // rows of the 16 edges as B, so that lane 16 h + c ends with the four
-      // consecutive columns 16 ti + 4 h .. + 3 of edge c's grad_x row, stored as
-      // they are; formed after G, so that its accumulators are not live beside
-      // G's operands
+      // consecutive columns 16 ti + 4 h .. + 3 of edge c's grad_x row; formed
+      // after G, so that its accumulators are not live beside G's operands
       f32x4 gA[NT];
 #pragma unroll
       for (int tk = 0; tk < NT; ++tk)
@@ -1265,8 +1266,23 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             D = __builtin_amdgcn_mfma_f32_16x16x4f32(m[cw][(tk * NT + ti) * 4 + r], gA[tk][r], D, 0, 0, 0);
-        store_tile_f4(ro, uint32_t(c) * EDGE_BYTES + uint32_t(D1 * cw + 16 * ti + 4 * h) * 4u, D);
+        Dout[cw * NT + ti] = D;
       }
+    }
+    // Dout[0] holds columns 4 h .. + 3 of edge c's 32-float row, Dout[1] columns
+    // 16 + 4 h .. + 3.  Lanes c and c + 8 trade one of them (a DPP rotation by 8
+    // within each row of 16 lanes), so that each store writes eight whole rows
+    // of 128 bytes: the first edges c % 8, the second edges c % 8 + 8.
+    {
+      const bool lo = c < 8;
+      const f32x4 snd = lo ? Dout[1] : Dout[0];
+      f32x4 rcv;
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        rcv[r] = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(snd[r]), 0x128, 0xf, 0xf, false));
+      const uint32_t col = uint32_t((lo ? 0 : 16) + 4 * h) * 4u, e1 = uint32_t(c & 7);
+      store_tile_f4(ro, e1 * EDGE_BYTES + col, lo ? Dout[0] : rcv);
+      store_tile_f4(ro, (e1 + 8u) * EDGE_BYTES + col, lo ? rcv : Dout[1]);
     }
     lds_sync<1>();  // the tile's LDS reads are done: the area is free again
   };
