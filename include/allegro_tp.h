@@ -77,7 +77,8 @@ enum {
   ALLEGRO_E_INVALID = -1,     /* bad argument (pointer, size, alignment, CSR) */
   ALLEGRO_E_UNSUPPORTED = -2, /* lmax or U outside the compiled set */
   ALLEGRO_E_HIP = -3,         /* HIP runtime or launch failure */
-  ALLEGRO_E_NOMEM = -4        /* plan allocation failed */
+  ALLEGRO_E_NOMEM = -4,       /* plan allocation failed */
+  ALLEGRO_E_TIMEOUT = -5      /* a bounded wait on the device ran out (reported under ALLEGRO_VALIDATE) */
 };
 
 enum {
@@ -155,7 +156,14 @@ int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t
  * allegro_tp_backward_workspace() bytes, 16-byte aligned, overwritten (no
  * clearing needed); calls that share a workspace must not overlap.  N == 0
  * sets grad_path_w to zero.  Errors as for allegro_tp_backward, plus
- * ALLEGRO_E_INVALID for a missing or too small workspace. */
+ * ALLEGRO_E_INVALID for a missing or too small workspace.  At lmax 3 the
+ * matrix-core kernel's waves hand work to each other through bounded waits
+ * (about a second each); one that ran out (a stalled wave; it does not happen
+ * in a working kernel) makes the kernel finish without waiting further, and
+ * its outputs are then not valid: with ALLEGRO_VALIDATE the call waits for the
+ * kernel and returns ALLEGRO_E_TIMEOUT.  For tests of that path, a plan
+ * created while the environment variable ALLEGRO_SIMULATE_HANDOVER_TIMEOUT is
+ * set gives up every such wait at once. */
 int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
                               const float *x, const float *env, const float *path_w,
                               const float *grad_out, const float *w, const float *Y,

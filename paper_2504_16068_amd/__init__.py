@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     ALLEGRO_E_HIP,
     ALLEGRO_E_INVALID,
     ALLEGRO_E_NOMEM,
+    ALLEGRO_E_TIMEOUT,
     ALLEGRO_E_UNSUPPORTED,
     ALLEGRO_FULL_PARITY,
     ALLEGRO_OK,

@@ -21,6 +21,7 @@ ALLEGRO_E_INVALID = -1
 ALLEGRO_E_UNSUPPORTED = -2
 ALLEGRO_E_HIP = -3
 ALLEGRO_E_NOMEM = -4
+ALLEGRO_E_TIMEOUT = -5
 ALLEGRO_FULL_PARITY = 1
 ALLEGRO_DETERMINISTIC = 2
 ALLEGRO_VALIDATE = 4

@@ -817,10 +817,11 @@ struct MfmaShape {
 };
 
 // LDS position of element (row e, column k) of a tile of 32-float rows: the
-// 16-byte column k / 4 XOR f(e), f(e) = (e & 7) ^ 4 (e & 1), so that 8
-// consecutive rows read at one 16-byte column, two rows 4 s + h, 4 s + h + 1
-// read at 16 consecutive columns, or one row read in 16-byte pieces, hit
-// distinct banks.
+// 16-byte column k / 4 XOR f(e), f(e) = (e & 7) ^ 4 (e & 1), so that the 16
+// rows of a tile read at one logical 16-byte column (the grad_x operand: lane
+// c reads row c) hit 16 distinct bank groups, while a row stays one 128-byte
+// span (the staging writes, and the G operands' column pairs, 16 lanes to a
+// row).
 __device__ __forceinline__ int swz32(int e, int k) {
   const int f = (e & 7) ^ ((e & 1) << 2);
   return e * 32 + ((((k >> 2) ^ f)) << 2) + (k & 3);
@@ -846,16 +847,25 @@ struct Handover {
   int m_ready, m_taken, g_written, g_taken;
 };
 constexpr int kSpinLimit = 1 << 24;  // polls before a wait gives up (about a second)
+constexpr int kHandoverTimeout = 2;  // bit of the plan's device status word: a handover wait ran out
+
+// Where a handover wait gives up and reports it: after `limit` polls; `status`
+// (a device word, or null) gets kHandoverTimeout.
+struct WaitCfg {
+  int limit;
+  int *status;
+};
 
 // Waits until *c >= v (acquire); false if the workgroup has stopped or the wait
-// ran out, in which case the workgroup is stopped.
-__device__ __forceinline__ bool wait_for(int *c, int v, int *stop) {
-  for (int n = 0; n < kSpinLimit; ++n) {
+// ran out, in which case the workgroup is stopped and the timeout reported.
+__device__ __forceinline__ bool wait_for(int *c, int v, int *stop, WaitCfg cfg) {
+  for (int n = 0; n < cfg.limit; ++n) {
     if (__hip_atomic_load(c, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= v) return true;
     if (__hip_atomic_load(stop, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) return false;
     __builtin_amdgcn_s_sleep(1);
   }
   __hip_atomic_store(stop, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (cfg.status) __hip_atomic_fetch_or(cfg.status, kHandoverTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return false;
 }
 __device__ __forceinline__ void post(int *c, int v) {
@@ -895,7 +905,7 @@ template <bool FULL, int U, bool WG>
 __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     int64_t N, const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
     const float *__restrict__ path_w, const float *__restrict__ g, float *__restrict__ grad_x,
-    float *__restrict__ grad_env, float *__restrict__ pw_part) {
+    float *__restrict__ grad_env, float *__restrict__ pw_part, WaitCfg wcfg) {
   using Sh = MfmaShape<FULL>;
   using Tab = typename Sh::Tab;
   constexpr int D1 = Sh::D1, D2 = Sh::D2, NT = Sh::NT, S = Sh::S, NP = Sh::NP, CPW = Sh::CPW;
@@ -1099,13 +1109,13 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     while (have) {
       const int64_t cn = walk.n;
       const int cu0 = walk.u0;
-      if (!wait_for(&hv.m_taken, k - 1, &stop)) return;  // the wave has taken the previous M
+      if (!wait_for(&hv.m_taken, k - 1, &stop, wcfg)) return;  // the wave has taken the previous M
       build_m();
       post(&hv.m_ready, k);
       have = walk.next(row_ptr, on_empty);
       if (have) load_params(walk.n, walk.u0);
       if (k > 0) {
-        if (!wait_for(&hv.g_written, k - 1, &stop)) return;
+        if (!wait_for(&hv.g_written, k - 1, &stop, wcfg)) return;
         contract_g(prev_n, prev_u0);
         post(&hv.g_taken, k - 1);
       }
@@ -1114,7 +1124,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
       prev_u0 = cu0;
       ++k;
     }
-    if (k > 0 && wait_for(&hv.g_written, k - 1, &stop)) {
+    if (k > 0 && wait_for(&hv.g_written, k - 1, &stop, wcfg)) {
       contract_g(prev_n, prev_u0);
       post(&hv.g_taken, k - 1);
     }
@@ -1130,7 +1140,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
   int64_t feb = walk.eb;
   // the ring of tiles in flight: slot d holds a tile and its identity
   f32x4 vx[DEPTH][LJ], vg[DEPTH][LJ];
-  int64_t s_n[DEPTH], s_eb[DEPTH], s_e1[DEPTH];
+  int64_t s_eb[DEPTH], s_e1[DEPTH];
   int s_u0[DEPTH];
   bool s_valid[DEPTH], s_first[DEPTH];
   // Every tile, valid or not, issues the same memory instructions (an empty
@@ -1139,7 +1149,6 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
   // wait for a tile's data waits for that tile's loads only.
   auto fetch = [&](int d) {
     s_valid[d] = fvalid;
-    s_n[d] = walk.n;
     s_u0[d] = walk.u0;
     s_eb[d] = feb;
     s_e1[d] = walk.e1;
@@ -1174,7 +1183,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
   int k = -1;  // index of that pair in the wave's sequence
   // G of pair k to the helper (after it has contracted pair k - 1's)
   auto hand_g = [&]() {
-    wait_for(&hv.g_taken, k - 1, &stop);
+    wait_for(&hv.g_taken, k - 1, &stop, wcfg);
 #pragma unroll
     for (int cw = 0; cw < CPW; ++cw)
 #pragma unroll
@@ -1186,7 +1195,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     if (s_valid[d] && s_first[d]) {
       if (k >= 0) hand_g();
       ++k;
-      wait_for(&hv.m_ready, k, &stop);
+      wait_for(&hv.m_ready, k, &stop, wcfg);
 #pragma unroll
       for (int cw = 0; cw < CPW; ++cw) {
 #pragma unroll
@@ -1314,9 +1323,6 @@ __device__ __forceinline__ Dual dmul(const Dual &a, const Dual &b) {
   return {a.v * b.v, {a.v * b.g[0] + a.g[0] * b.v, a.v * b.g[1] + a.g[1] * b.v, a.v * b.g[2] + a.g[2] * b.v}};
 }
 __device__ __forceinline__ Dual dscale(double c, const Dual &a) { return {c * a.v, {c * a.g[0], c * a.g[1], c * a.g[2]}}; }
-__device__ __forceinline__ Dual dadd(const Dual &a, const Dual &b) {
-  return {a.v + b.v, {a.g[0] + b.g[0], a.g[1] + b.g[1], a.g[2] + b.g[2]}};
-}
 __device__ __forceinline__ Dual dsub(const Dual &a, const Dual &b) {
   return {a.v - b.v, {a.g[0] - b.g[0], a.g[1] - b.g[1], a.g[2] - b.g[2]}};
 }
@@ -1495,7 +1501,7 @@ bool misaligned(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) !
 using EnvFn = void (*)(dim3, hipStream_t, int64_t, const int64_t *, const float *, const float *, float *);
 using FwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, float *);
 using BwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const float *, const float *, const float *,
-                       const float *, const float *, float *, float *, float *, float *, float *);
+                       const float *, const float *, float *, float *, float *, float *, float *, WaitCfg);
 
 template <int U, int D2, bool DET>
 void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const float *w, const float *Y, float *env) {
@@ -1545,15 +1551,15 @@ unsigned mfma_grid(int64_t N) {
 template <class Core, int U, bool WG>
 void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, const float *env, const float *pw,
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
-                float *pw_part) {
+                float *pw_part, WaitCfg wcfg) {
   if constexpr (Core::LMAX >= 3 && WG) {
     // training backward at lmax 3: grad_x, grad_env and the path-weight rows on
     // the matrix cores (one read of x and g), then the embedding VJP from the
     // complete grad_env.  The inference backward stays on the direct kernel,
-    // which is faster there (10.6 against 12.6 ms on 20,000 centers, U = 128).
+    // which is faster there (10.3 against 12.0 ms on 20,000 centers, U = 128).
     const int64_t N = grid.x;
     hipLaunchKernelGGL((tp_mfma_bwd_kernel<Core::FULL, U, WG>), dim3(mfma_grid<Core::FULL, U, WG>(N)),
-                       dim3(MfmaShape<Core::FULL>::THREADS), 0, s, N, rp, x, env, pw, g, gx, genv, pw_part);
+                       dim3(MfmaShape<Core::FULL>::THREADS), 0, s, N, rp, x, env, pw, g, gx, genv, pw_part, wcfg);
     hipLaunchKernelGGL((embedding_vjp_kernel<U, Core::D2, 4>), grid, dim3(kWave * 4), 0, s, rp, genv, w, Y, gw, gy);
   } else {
     hipLaunchKernelGGL((tp_backward_kernel<Core, U, WG>), grid, dim3(kWave * TPWaves<Core, U>::bwd(WG)), 0, s, rp, x,
@@ -1620,8 +1626,9 @@ int check_tensor(const void *ptr, const char *name) {
   return ALLEGRO_OK;
 }
 
-int validate_csr(allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_ptr, hipStream_t s) {
-  std::lock_guard<std::mutex> lock(p->validate_mu);
+// The device CSR check of ALLEGRO_VALIDATE; the caller holds p->validate_mu.
+// On success the status word is zero.
+int validate_csr_locked(allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_ptr, hipStream_t s) {
   hipLaunchKernelGGL(zero_word_kernel, dim3(1), dim3(1), 0, s, p->status);
   const int64_t blocks = std::min<int64_t>((N + 256) / 256, 4096);
   hipLaunchKernelGGL(csr_check_kernel, dim3(unsigned(blocks)), dim3(256), 0, s, N, E, row_ptr, p->status);
@@ -1631,6 +1638,25 @@ int validate_csr(allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_pt
     return fail(ALLEGRO_E_HIP, "CSR validation failed to run: %s", hipGetErrorString(hipGetLastError()));
   if (host) return fail(ALLEGRO_E_INVALID, "row_ptr is not a valid CSR pointer for N=%lld, E=%lld", (long long)N,
                         (long long)E);
+  return ALLEGRO_OK;
+}
+
+int validate_csr(allegro_tp_plan *p, int64_t N, int64_t E, const int64_t *row_ptr, hipStream_t s) {
+  std::lock_guard<std::mutex> lock(p->validate_mu);
+  return validate_csr_locked(p, N, E, row_ptr, s);
+}
+
+// After the launches of a validated training backward (p->validate_mu held, the
+// status word zeroed by the CSR check): waits for them and reports a handover
+// wait of the matrix-core kernel that ran out.
+int check_handover_locked(allegro_tp_plan *p, hipStream_t s, const char *what) {
+  int host = 0;
+  if (hipMemcpyAsync(&host, p->status, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess)
+    return fail(ALLEGRO_E_HIP, "%s: reading the device status failed: %s", what, hipGetErrorString(hipGetLastError()));
+  if (host & kHandoverTimeout)
+    return fail(ALLEGRO_E_TIMEOUT, "%s: a wait between the matrix-core kernel's waves ran out; the outputs are not valid",
+                what);
   return ALLEGRO_OK;
 }
 
@@ -1658,6 +1684,12 @@ static bool simulated_alloc_failure(const char *what) {
   return v && std::strcmp(v, what) == 0;
 }
 
+// Failure injection for tests: with ALLEGRO_SIMULATE_HANDOVER_TIMEOUT set (to
+// anything) at plan creation, every wait between the waves of the matrix-core
+// backward gives up at once, as if the partner wave had stalled; the kernel
+// still runs to its end, and a validating plan reports ALLEGRO_E_TIMEOUT.
+static bool simulated_handover_timeout() { return std::getenv("ALLEGRO_SIMULATE_HANDOVER_TIMEOUT") != nullptr; }
+
 int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags) {
   if (!plan) return fail(ALLEGRO_E_INVALID, "plan output pointer is NULL");
   *plan = nullptr;
@@ -1671,6 +1703,7 @@ int allegro_tp_plan_create(allegro_tp_plan **plan, int lmax, int U, int flags) {
   p->lmax = lmax;
   p->U = U;
   p->flags = flags;
+  if (simulated_handover_timeout()) p->spin_limit = 0;
   try {
     if (simulated_alloc_failure("table")) throw std::bad_alloc();
     p->table = allegro::build_table(lmax, (flags & ALLEGRO_FULL_PARITY) != 0);
@@ -1785,7 +1818,8 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
   if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
   const Kernels k = select(plan);
   if (!k.bwd) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
-  k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, nullptr);
+  k.bwd(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, nullptr,
+        WaitCfg{plan->spin_limit, nullptr});
   return after_launch("allegro_tp_backward");
 }
 
@@ -1831,18 +1865,27 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
                 (rc = check_tensor(grad_w, "grad_w")) || (rc = check_tensor(grad_Y, "grad_Y"))))
     return rc;
   auto *mp = const_cast<allegro_tp_plan *>(plan);
-  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  // validated: the status word stays locked from the CSR check to the report
+  // of the handover waits
+  const bool validate = (plan->flags & ALLEGRO_VALIDATE) != 0;
+  std::unique_lock<std::mutex> vlock;
+  if (validate) {
+    vlock = std::unique_lock<std::mutex>(mp->validate_mu);
+    if ((rc = validate_csr_locked(mp, N, E, row_ptr, s))) return rc;
+  }
   const Kernels k = select(plan);
   if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
   float *part = static_cast<float *>(workspace);
   float *chunks = part + N * cols;
-  k.bwd_wg(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, part);
+  k.bwd_wg(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, part,
+           WaitCfg{plan->spin_limit, validate ? plan->status : nullptr});
   if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
   const unsigned cb = unsigned((cols + 255) / 256);
   hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
   hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w,
                      pw_rows_np(plan));
-  return after_launch("allegro_tp_backward_train");
+  if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
+  return validate ? check_handover_locked(mp, s, "allegro_tp_backward_train") : ALLEGRO_OK;
 }
 
 int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
@@ -1875,7 +1918,13 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
   float *scr = nullptr;
   if ((rc = noalloc_scratch(&scr))) return rc;
   auto *mp = const_cast<allegro_tp_plan *>(plan);
-  if ((plan->flags & ALLEGRO_VALIDATE) && (rc = validate_csr(mp, N, E, row_ptr, s))) return rc;
+  const bool validate = (plan->flags & ALLEGRO_VALIDATE) != 0;
+  std::unique_lock<std::mutex> vlock;
+  if (validate) {
+    vlock = std::unique_lock<std::mutex>(mp->validate_mu);
+    if ((rc = validate_csr_locked(mp, N, E, row_ptr, s))) return rc;
+  }
+  const WaitCfg wcfg{plan->spin_limit, validate ? plan->status : nullptr};
   const Kernels k = select(plan);
   if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
   // scratch: per-center rows of one chunk, the 128 range sums of a chunk, then
@@ -1888,7 +1937,7 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
     // the chunk's centers as a CSR of their own: row_ptr values stay absolute
     // edge indices, center-indexed tensors are offset to the chunk's first center
     k.bwd_wg(dim3(unsigned(n1 - n0)), s, row_ptr + n0, x, env + n0 * ud2, path_w, grad_out, w, Y, grad_x,
-             grad_env + n0 * ud2, grad_w, grad_Y, part);
+             grad_env + n0 * ud2, grad_w, grad_Y, part, wcfg);
     hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, n1 - n0, cols, part, ranges);
     hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, ranges,
                        chunk_rows + c * cols, 0);
@@ -1896,7 +1945,8 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
   }
   hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, int(n_chunks), cols, chunk_rows,
                      grad_path_w, pw_rows_np(plan));
-  return after_launch("allegro_tp_backward_train_noalloc");
+  if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
+  return validate ? check_handover_locked(mp, s, "allegro_tp_backward_train_noalloc") : ALLEGRO_OK;
 }
 
 // One edge per thread in 256-thread blocks; the grid's x extent stays below 2^31.

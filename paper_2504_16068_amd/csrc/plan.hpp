@@ -13,6 +13,9 @@ struct allegro_tp_plan {
   allegro::TPTable table;
   int *status = nullptr;  // device word for ALLEGRO_VALIDATE
   std::mutex validate_mu;
+  // polls before a wait between the waves of the matrix-core backward gives
+  // up (0 only to test that path: every such wait then gives up at once)
+  int spin_limit = 1 << 24;
 };
 
 namespace allegro_internal {

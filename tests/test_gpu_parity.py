@@ -456,6 +456,37 @@ def test_train_backward_without_edges(at):
         assert torch.count_nonzero(gpw).item() == 0 and torch.count_nonzero(genv).item() == 0
 
 
+def test_handover_timeout_is_reported_and_ends(at, monkeypatch):
+    """With the handover waits of the lmax-3 matrix-core backward forced to give
+    up at once (a plan created under ALLEGRO_SIMULATE_HANDOVER_TIMEOUT), the
+    kernel still runs to its end: a validating plan reports ALLEGRO_E_TIMEOUT
+    (both entry points), a plain one returns; a normal plan afterwards is exact."""
+    lmax, full, U, degrees = 3, True, 64, [1, 0, 9, 70, 33]
+    data = _synthetic(lmax, full, U, degrees, seed=41)
+    rp, xd, wd, yd, pwd, gd = (_t(a) for a in data)
+    _note("[gpu] handover timeout forced from the host: lmax 3, U 64")
+    monkeypatch.setenv("ALLEGRO_SIMULATE_HANDOVER_TIMEOUT", "1")
+    stalled = _plan(at, lmax, U, full, validate=True)
+    stalled_plain = _plan(at, lmax, U, full)
+    monkeypatch.delenv("ALLEGRO_SIMULATE_HANDOVER_TIMEOUT")
+    normal = _plan(at, lmax, U, full, validate=True)
+    env = at.allegro_env_embed(normal, rp, wd, yd)
+    with pytest.raises(at.AllegroError) as ex:
+        _train(at, stalled, rp, xd, env, pwd, gd, wd, yd)
+    assert ex.value.code == at.ALLEGRO_E_TIMEOUT and "ran out" in str(ex.value)
+    with pytest.raises(at.AllegroError) as ex:
+        at.allegro_tp_backward_train_noalloc(stalled, rp, xd, env, pwd, gd, wd, yd)
+    assert ex.value.code == at.ALLEGRO_E_TIMEOUT
+    _train(at, stalled_plain, rp, xd, env, pwd, gd, wd, yd)  # returns; its outputs are not valid
+    (gx, genv, gw, gy, gpw), _ = _train(at, normal, rp, xd, env, pwd, gd, wd, yd)
+    t = otp.TensorProduct(lmax, full)
+    renv = otp.env_embed(data[0], data[2], data[3])
+    ref = t.backward(data[0], data[1], renv, data[4], data[5], data[2], data[3])
+    for got, r, blocks in zip((gx, genv, gw, gy), ref, (t.x_slices, t.env_slices, None, t.env_slices)):
+        assert block_rel_err(got.cpu().numpy(), r, blocks) <= BWD_TOL
+    assert block_rel_err(gpw.cpu().numpy(), t.path_weight_grad(data[0], data[1], renv, data[5])) <= BWD_TOL
+
+
 def test_train_backward_rejects_small_workspace(at):
     plan = _plan(at, 1, 16, False)
     rp = torch.tensor([0, 2], dtype=torch.int64, device=DEV)
