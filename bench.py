@@ -173,6 +173,50 @@ def pmc_summary(fetch_csv: str, write_csv: str, workload: str, key: str):
 
 # ------------------------------------------------------------------ probes
 
+def pattern_probe(torch, dev, reps=5):
+    """The lmax-3 matrix-core backward's tile stream without its arithmetic
+    (csrc/stream_probe.hip, pattern_probe): c = a + b over [E][U][32] fp32 on
+    the high-order edges, with 128-, 256- and 512-byte rows per wave, at one
+    and two workgroups of 8 waves per compute unit.  ms and TB/s per variant."""
+    import ctypes
+
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2504_16068_amd", "libstream_probe.so"))
+    lib.pattern_probe.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint, ctypes.c_void_p]
+    graph = workloads.make_graph("high_order")
+    n, e, u = graph.n_atoms, graph.n_edges, graph.config.U
+    a = torch.rand(e * u * 32, device=dev)
+    b = torch.rand(e * u * 32, device=dev)
+    c = torch.empty_like(a)
+    rp = torch.from_numpy(graph.row_ptr).to(dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    nbytes = 3 * e * u * 32 * 4
+    names = ["128B rows, 4 tiles", "128B rows, 6 tiles", "256B rows, 2 tiles", "256B rows, 4 tiles",
+             "512B rows, 2 tiles"]
+    out = {"workload": f"high_order: {e} edges, U={u}, rows of 32 floats per channel", "bytes": nbytes}
+    for variant, name in enumerate(names):
+        for per_cu in (1, 2):
+            def run():
+                rc = lib.pattern_probe(variant, n, u, rp.data_ptr(), a.data_ptr(), b.data_ptr(), c.data_ptr(),
+                                       cus * per_cu, stream)
+                if rc:
+                    raise RuntimeError(f"pattern_probe failed ({rc})")
+            run()
+            torch.cuda.synchronize()
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record()
+            for _ in range(reps):
+                run()
+            t1.record()
+            torch.cuda.synchronize()
+            ms = t0.elapsed_time(t1) / reps
+            out[f"{name}, {per_cu} workgroup(s) per CU"] = {"ms": ms, "TBps": nbytes / ms / 1e9}
+    if not torch.allclose(c[:4096], a[:4096] + b[:4096]):
+        raise RuntimeError("pattern_probe wrote wrong sums")
+    return out
+
+
 def stream_probes(torch, dev, n_bytes=4 << 30, reps=5):
     """Rates (GB/s of bytes moved) of plain streams over 4 GiB per tensor, outside
     every cache: read only, one read + one write, two reads + one write, each the
@@ -512,6 +556,8 @@ def main():
     ap.add_argument("--no-large", action="store_true", help="skip the large-system record")
     ap.add_argument("--layer-only", action="store_true",
                     help="time only the Allegro layer and print its record (no step, no JSON bench line)")
+    ap.add_argument("--pattern-probe", action="store_true",
+                    help="time the lmax-3 matrix-core backward's access pattern alone (high-order edges) and exit")
     ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write a calibrated traffic record from two rocprofv3 --pmc runs and exit")
     ap.add_argument("--pmc-kernel", default="tp_backward", choices=sorted(TRAFFIC_KERNELS))
@@ -524,7 +570,7 @@ def main():
               "communication inside the path; each GPU would run this on its own share.", file=sys.stderr)
         sys.exit(2)
 
-    cpu = None if args.no_cpu_baseline or args.layer_only else cpu_baseline()
+    cpu = None if args.no_cpu_baseline or args.layer_only or args.pattern_probe else cpu_baseline()
     if cpu is not None:
         note(f"cpu baseline done: {cpu['value']:.3g} edges/s on {cpu['cores']} processes")
 
@@ -535,6 +581,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.layer_only:
         print(json.dumps({"allegro_layer": time_layer(torch, at, dev, max(3, min(args.steps, 10)))}), flush=True)
+        return
+    if args.pattern_probe:
+        print(json.dumps({"pattern_probe": pattern_probe(torch, dev)}), flush=True)
         return
     probes = stream_probes(torch, dev)
     note("stream probes done: " + ", ".join(f"{k} {v['GBps']:.0f} GB/s" for k, v in probes.items()))

@@ -52,7 +52,85 @@ void launch(int unroll, unsigned blocks, hipStream_t s, const f32x4 *a, const f3
   else hipLaunchKernelGGL((stream_kernel<PATTERN, 4>), dim3(blocks), dim3(256), 0, s, a, b, c, n);
 }
 
+// Access pattern of the lmax-3 matrix-core backward's tile stream, without its
+// arithmetic: c = a + b over tensors [E][U][32] (fp32), a persistent grid of
+// workgroups of 8 waves, each wave walking its own sequence of (center,
+// channel group) pairs round robin, 16 edges per tile, DEPTH tiles loaded
+// before they are stored, ROWF4 float4 of an edge's row per wave (8: one
+// channel of 32 floats, 128 bytes; 16: two; 32: four).  Rows past a center's
+// edges lie past the buffer descriptor's range: loads read zeros, stores drop.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void *p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), short(0), int(bytes), 0x00020000);
+}
+
+template <int ROWF4, int DEPTH>
+__global__ __launch_bounds__(512) void pattern_kernel(int64_t N, int U, const int64_t *__restrict__ row_ptr,
+                                                      const float *__restrict__ a, const float *__restrict__ b,
+                                                      float *__restrict__ c) {
+  constexpr int LR = 64 / ROWF4;  // rows per 16-byte load instruction
+  constexpr int LJ = 16 / LR;     // load instructions per tensor and tile
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / 64), lane = int(threadIdx.x) % 64;
+  const int groups = U * 8 / ROWF4;  // channel groups per center (8 float4 per channel)
+  const int64_t total = int64_t(gridDim.x) * 8, pairs = N * groups;
+  const uint32_t row_bytes = uint32_t(U) * 128u;
+  const uint32_t voff = uint32_t(lane / ROWF4) * row_bytes + uint32_t(lane % ROWF4) * 16u;
+  for (int64_t fq = int64_t(blockIdx.x) * 8 + wave; fq < pairs; fq += total) {
+    const int64_t n = fq / groups;
+    const int gi = int(fq % groups);
+    const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+    for (int64_t e = e0; e < e1; e += 16 * DEPTH) {
+      f32x4 va[DEPTH][LJ], vb[DEPTH][LJ];
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        const int64_t te = e + 16 * d;
+        const uint32_t bytes = te < e1 ? uint32_t(e1 - te < 16 ? e1 - te : 16) * row_bytes : 0u;
+        const int64_t base = te * U * 32 + int64_t(gi) * ROWF4 * 4;
+        const auto ra = row_rsrc(a + base, bytes), rb = row_rsrc(b + base, bytes);
+#pragma unroll
+        for (int j = 0; j < LJ; ++j) {
+          const int o = int(voff + uint32_t(LR * j) * row_bytes);
+          va[d][j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, o, 0, 2));
+          vb[d][j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(rb, o, 0, 2));
+        }
+      }
+#pragma unroll
+      for (int d = 0; d < DEPTH; ++d) {
+        const int64_t te = e + 16 * d;
+        const uint32_t bytes = te < e1 ? uint32_t(e1 - te < 16 ? e1 - te : 16) * row_bytes : 0u;
+        const auto rc = row_rsrc(c + te * U * 32 + int64_t(gi) * ROWF4 * 4, bytes);
+#pragma unroll
+        for (int j = 0; j < LJ; ++j)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, va[d][j] + vb[d][j]), rc,
+                                                 int(voff + uint32_t(LR * j) * row_bytes), 0, 2);
+      }
+    }
+  }
+}
+
 }  // namespace
+
+// The access-pattern probe: variant 0 = 128-byte rows, 4 tiles in flight;
+// 1 = 128-byte rows, 6 tiles; 2 = 256-byte rows, 2 tiles; 3 = 256-byte rows,
+// 4 tiles; 4 = 512-byte rows, 2 tiles.  a, b, c hold row_ptr[N] rows of
+// U * 32 floats; U is 64 or 128.  Returns 0, -1 for bad arguments, -3 on a
+// launch error.
+extern "C" int pattern_probe(int variant, int64_t N, int U, const int64_t *row_ptr, const void *a, const void *b,
+                             void *c, unsigned blocks, void *stream) {
+  if (N <= 0 || (U != 64 && U != 128) || !row_ptr || !a || !b || !c || blocks == 0) return -1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float *pa = static_cast<const float *>(a), *pb = static_cast<const float *>(b);
+  float *pc = static_cast<float *>(c);
+  switch (variant) {
+    case 0: hipLaunchKernelGGL((pattern_kernel<8, 4>), dim3(blocks), dim3(512), 0, s, N, U, row_ptr, pa, pb, pc); break;
+    case 1: hipLaunchKernelGGL((pattern_kernel<8, 6>), dim3(blocks), dim3(512), 0, s, N, U, row_ptr, pa, pb, pc); break;
+    case 2: hipLaunchKernelGGL((pattern_kernel<16, 2>), dim3(blocks), dim3(512), 0, s, N, U, row_ptr, pa, pb, pc); break;
+    case 3: hipLaunchKernelGGL((pattern_kernel<16, 4>), dim3(blocks), dim3(512), 0, s, N, U, row_ptr, pa, pb, pc); break;
+    case 4: hipLaunchKernelGGL((pattern_kernel<32, 2>), dim3(blocks), dim3(512), 0, s, N, U, row_ptr, pa, pb, pc); break;
+    default: return -1;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 // n_f4 float4 per stream; blocks of 256 threads (for pattern 0, c must hold
 // blocks * 256 floats).  Returns 0, or -1 for bad arguments, -3 on a launch
