@@ -214,6 +214,30 @@ def pattern_probe(torch, dev, reps=5):
             out[f"{name}, {per_cu} workgroup(s) per CU"] = {"ms": ms, "TBps": nbytes / ms / 1e9}
     if not torch.allclose(c[:4096], a[:4096] + b[:4096]):
         raise RuntimeError("pattern_probe wrote wrong sums")
+    del a, b, c
+    # the direct kernels' traversal at the headline: one workgroup of 16 waves
+    # per center copying whole 4.6 KB edge rows (x -> out, no arithmetic)
+    lib.center_copy_probe.argtypes = [ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    hg = workloads.make_graph("headline")
+    x = torch.rand(hg.n_edges * 64 * 18, device=dev)
+    y = torch.empty_like(x)
+    hrp = torch.from_numpy(hg.row_ptr).to(dev)
+    run = lambda: lib.center_copy_probe(hg.n_atoms, hrp.data_ptr(), x.data_ptr(), y.data_ptr(), stream)
+    if run():
+        raise RuntimeError("center_copy_probe failed")
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        run()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    if not torch.equal(x, y):
+        raise RuntimeError("center_copy_probe copied wrong values")
+    cb = 2 * x.numel() * 4
+    out["headline per-center copy (16 waves per center, 4.6 KB rows)"] = {"ms": ms, "TBps": cb / ms / 1e9}
     return out
 
 

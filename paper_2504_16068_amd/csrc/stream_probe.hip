@@ -108,7 +108,41 @@ __global__ __launch_bounds__(512) void pattern_kernel(int64_t N, int U, const in
   }
 }
 
+// A plain copy out = x of edge rows of RF4 float4 with the direct kernels'
+// traversal: one workgroup of NW waves per center, each wave copying whole
+// edge rows of its center round robin (non-temporal 16-byte accesses).
+template <int NW, int RF4>
+__global__ __launch_bounds__(64 * NW) void center_copy_kernel(const int64_t *__restrict__ row_ptr,
+                                                              const f32x4 *__restrict__ x, f32x4 *__restrict__ out) {
+  constexpr int PER = (RF4 + 63) / 64;
+  const int wave = int(threadIdx.x) / 64, lane = int(threadIdx.x) % 64;
+  const int64_t n = blockIdx.x, e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  for (int64_t e = e0 + wave; e < e1; e += NW) {
+    f32x4 v[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = lane + 64 * i;
+      if (f < RF4) v[i] = __builtin_nontemporal_load(x + e * RF4 + f);
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = lane + 64 * i;
+      if (f < RF4) __builtin_nontemporal_store(v[i], out + e * RF4 + f);
+    }
+  }
+}
+
 }  // namespace
+
+// The per-center copy probe: rows of U * 18 floats (U = 64: 288 float4, the
+// headline's x rows), one workgroup of 16 waves per center for N centers.
+// Returns 0, -1 for bad arguments, -3 on a launch error.
+extern "C" int center_copy_probe(int64_t N, const int64_t *row_ptr, const void *x, void *out, void *stream) {
+  if (N <= 0 || !row_ptr || !x || !out) return -1;
+  hipLaunchKernelGGL((center_copy_kernel<16, 288>), dim3(unsigned(N)), dim3(1024), 0, static_cast<hipStream_t>(stream),
+                     row_ptr, static_cast<const f32x4 *>(x), static_cast<f32x4 *>(out));
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
 
 // The access-pattern probe: variant 0 = 128-byte rows, 4 tiles in flight;
 // 1 = 128-byte rows, 6 tiles; 2 = 256-byte rows, 2 tiles; 3 = 256-byte rows,
