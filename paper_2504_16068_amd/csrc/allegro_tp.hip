@@ -379,57 +379,87 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 // is in flight while the current one is computed.  Per edge and channel this
 // takes about 900 FMAs instead of about 2,000 instructions, which makes the
 // lmax-3 forward HBM-bound.
+// s_waitcnt operand that waits until at most n vector memory operations of
+// the wave are outstanding (n < 64; lgkmcnt and expcnt left at their maxima):
+// the count's low four bits sit at bits 3:0, its high two at bits 15:14.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+// cache policy bits of a buffer access: non-temporal (streamed once)
+constexpr int kNonTemporal = 2;
+
 template <class Core>
 constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 
-// MF is the generated matrix TPMFwd (out = M x).
+// The per-center matrix forward at U = 128, d1 = 32, with the tiles brought
+// into LDS by direct buffer-to-LDS loads instead of through registers: the
+// registers the kernel leaves free hold one 32 KB tile, and at one workgroup
+// per compute unit one tile in flight leaves HBM latency-bound.  Four tile
+// buffers: tile k is multiplied while tiles k + 1 .. k + 3 load (96 KB in
+// flight per compute unit; the four buffers and the result tile fill the
+// 160 KB of LDS).  A load lands at the LDS address of its lane, so the source
+// addresses carry the layout: row r (slab r / 64, channel r % 64) holds its
+// 16-byte chunk q at position q ^ ((r / 2) mod 8), which keeps the rows'
+// 16-byte accesses (lane r reads row r, 16 lanes at a time over the 64 banks)
+// free of bank conflicts without padding; the result tile uses the same
+// layout.  The waits for a tile's loads are explicit (the compiler does not
+// track loads into LDS): every iteration issues the same number of loads and
+// stores (past the segment their descriptors have no range), so the number
+// issued after tile k's loads is fixed.
 template <class Core, int U, class MF>
-__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_matrix_kernel(
-    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
-    const float *__restrict__ path_w, float *__restrict__ out) {
+__device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_ptr, const float *__restrict__ x,
+                                               const float *__restrict__ env, const float *__restrict__ path_w,
+                                               float *__restrict__ out) {
+  typedef __attribute__((address_space(3))) void lds_void;
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   using L = Lanes<U>;
   constexpr int D1 = Core::D1, D2 = Core::D2, NW = MF::NW, ROWS = MF::ROWS;
-  constexpr int T = U > kWave ? 4 : 8;      // slabs per tile (32 or 64 KB; 8 at U = 128 would spill)
-  constexpr int RS = D1 + 4;                // padded LDS row stride (floats)
-  constexpr int R4 = D1 / 4;                // float4 per row
-  constexpr int SF4 = TileShape<D1>::SF4;   // float4 per slab
-  constexpr int TF4 = T * SF4;              // float4 per tile
+  constexpr int T = 4;                       // slabs per tile (32 KB)
+  constexpr int NB = 4;                      // tile buffers
+  constexpr int R4 = D1 / 4;                 // float4 per row
+  constexpr int TF4 = T * kWave * R4;        // float4 per tile
   constexpr int NT = NW * kWave;
-  constexpr int PER = (TF4 + NT - 1) / NT;  // float4 per thread and tile
-  static_assert(D1 % 4 == 0 && D1 == NW * ROWS, "rows of whole float4, split evenly over the waves");
-  __shared__ float4 xs4[T * kWave * RS / 4], os4[T * kWave * RS / 4];
-  float *xs = reinterpret_cast<float *>(xs4), *os = reinterpret_cast<float *>(os4);
+  constexpr int PER = TF4 / NT;              // loads (and stores) per thread and tile
+  constexpr uint32_t EDGE_BYTES = U * D1 * 4;
+  static_assert(D1 == 32 && U > kWave && TF4 % NT == 0 && D1 == NW * ROWS && ROWS == 4, "layout");
+  __shared__ float4 xb4[NB * TF4];
+  __shared__ float4 os4[TF4];  // the result tile, laid out as the tile buffers
+  const uint32_t xb_lds = uint32_t(reinterpret_cast<uintptr_t>((lds_void *)xb4));
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
-  const int64_t n_slabs = Slabs<U>::count(e1 - e0);
-  // float4 f of a tile starting at slab s0: its HBM index, or -1 past the segment
-  auto src = [&](int64_t s0, int f, int t) -> int64_t {
-    const int sl = f / SF4, in = f % SF4;
-    if (s0 + sl >= n_slabs) return -1;
-    if constexpr (U <= kWave) {
-      const int64_t base = Slabs<U>::first_edge(e0, s0) * (U * D1 / 4), end = e1 * (U * D1 / 4);
-      const int64_t g = base + f;
-      return g < end ? g : -1;
-    } else {
-      return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
-    }
-  };
+  const int64_t n_slabs = e1 - e0;  // one edge per slab (64 channels of one half)
+  const int64_t n_tiles = (n_slabs + T - 1) / T;
 #pragma unroll 1
   for (int t = 0; t < L::CPL; ++t) {
-    const int u = lane % L::LPE + t * kWave;
-    float4 v[PER];
-    auto fetch = [&](int64_t s0) {
-      const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    const int u = lane + t * kWave;
+    // tile k's rows of a [E][U][D1] tensor: a descriptor whose range ends at
+    // the segment's last slab (no range past it)
+    auto tile_rsrc = [&](const float *base, int64_t k) {
+      const int64_t s0 = k * T, cnt = s0 < n_slabs ? (n_slabs - s0 < T ? n_slabs - s0 : T) : 0;
+      const float *b = cnt ? base + ((e0 + s0) * U + t * kWave) * D1 : base;
+      return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(b), short(0), int(uint32_t(cnt) * EDGE_BYTES),
+                                               0x00020000);
+    };
+    // The loads into LDS are issued from inline assembly so that the
+    // compiler's wait insertion, which cannot tell the tile buffers apart,
+    // does not make every later LDS access wait for all of them.  LDS address
+    // of lane i: m0 + 16 i.
+    auto load_tile = [&](int64_t k) {
+      const int64_t s0 = k * T, cnt = s0 < n_slabs ? (n_slabs - s0 < T ? n_slabs - s0 : T) : 0;
+      const uint64_t b = cnt ? uint64_t(x + ((e0 + s0) * U + t * kWave) * D1) : uint64_t(x);
+      const u32x4 rs = {uint32_t(b), uint32_t(b >> 32) & 0xffffu, uint32_t(cnt) * EDGE_BYTES, 0x00020000u};
+      const uint32_t dst = xb_lds + uint32_t(k % NB) * uint32_t(TF4 * 16);
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
-        const int f = tid + NT * i;
-        const int64_t g = f < TF4 ? src(s0, f, t) : -1;
-        v[i] = g >= 0 ? load_stream(x4 + g) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const int blk = wave * PER + i, slot = blk * kWave + lane;
+        const int r = slot / R4, q = (slot % R4) ^ ((r >> 1) & 7);
+        const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(q) * 16;
+        asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
+                     :
+                     : "v"(voff), "s"(rs), "{m0}"(__builtin_amdgcn_readfirstlane(dst + uint32_t(blk * kWave * 16)))
+                     : "memory");
       }
     };
-    // M first: its weight loads would otherwise wait behind the tile's loads
-    // (one in-order counter covers both)
     float m[MF::MAXM];
     {
       CachedWeights wr;
@@ -438,42 +468,155 @@ __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per
       load_row<D2>(env + (n * U + u) * D2, er);
       MF::build(wave, er, wr, m);
     }
-    if (n_slabs > 0) fetch(0);
-    for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
-      // the tile from registers into LDS (padded rows), then the next tile's loads
+    // the loads above are complete before the tile loads start, so that no
+    // wait the compiler places for them covers the tile loads
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int f = tid + NT * i;
-        if (f < TF4) *reinterpret_cast<float4 *>(xs + (f / R4) * RS + 4 * (f % R4)) = v[i];
-      }
-      if (s0 + T < n_slabs) fetch(s0 + T);
-      lds_sync<NW>();
-      const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+    for (int k = 0; k < NB - 1; ++k) load_tile(k);
+#pragma unroll 1
+    for (int64_t k = 0; k < n_tiles; ++k) {
+      // loads and stores issued after tile k's loads, per wave: those of
+      // tiles k + 1 .. k + NB - 2 and the stores of the tiles in between
+      // (PER of each kind per tile)
+      if (k == 0)
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * PER));
+      else if (k == 1)
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(3 * PER));
+      else if (k == 2)
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(4 * PER));
+      else
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(5 * PER));
+      lds_sync<NW>();  // every wave's share of tile k is in LDS; tile k - 1's buffer is free
+      load_tile(k + NB - 1);
+      const float4 *xb = xb4 + int(k % NB) * TF4;
+      const int cnt = int(n_slabs - k * T < T ? n_slabs - k * T : T);
 #pragma unroll 1
       for (int sl = 0; sl < cnt; ++sl) {
         const int r = sl * kWave + lane;
         float xr[D1], o[ROWS];
 #pragma unroll
         for (int q = 0; q < R4; ++q) {
-          const float4 a = *reinterpret_cast<const float4 *>(xs + r * RS + 4 * q);
+          const float4 a = xb[r * R4 + (q ^ ((r >> 1) & 7))];
           xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
         }
         MF::apply(wave, xr, m, o);
-#pragma unroll
-        for (int k = 0; k < ROWS; ++k) os[r * RS + wave * ROWS + k] = o[k];
+        os4[r * R4 + (wave ^ ((r >> 1) & 7))] = make_float4(o[0], o[1], o[2], o[3]);
       }
       lds_sync<NW>();
-      float4 *o4 = reinterpret_cast<float4 *>(out);
+      const auto ro = tile_rsrc(out, k);
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
-        const int f = tid + NT * i;
-        const int64_t g = f < TF4 ? src(s0, f, t) : -1;
-        if (g >= 0) store_stream(*reinterpret_cast<const float4 *>(os + (f / R4) * RS + 4 * (f % R4)), o4 + g);
+        const int f = tid + NT * i, r = f / R4, c = f % R4;
+        const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(c) * 16;
+        const float4 v = os4[r * R4 + (c ^ ((r >> 1) & 7))];
+        __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y),
+                                                     __float_as_uint(v.z), __float_as_uint(v.w)},
+                                               ro, int(voff), 0, kNonTemporal);
       }
-      // the next iteration writes xs (read above, before the barrier) and then os
-      // only after its own barrier, by which every thread has read os here
     }
-    lds_sync<NW>();  // both tiles are free before the next channel half
+    // the loads of the tiles past the end (no range) before the buffers are
+    // reused or the workgroup ends
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_sync<NW>();
+  }
+}
+
+// MF is the generated matrix TPMFwd (out = M x).
+template <class Core, int U, class MF>
+__global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_matrix_kernel(
+    const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
+    const float *__restrict__ path_w, float *__restrict__ out) {
+  if constexpr (U > kWave && Core::D1 == 32) {
+    matrix_fwd_dma<Core, U, MF>(row_ptr, x, env, path_w, out);
+  } else {
+    using L = Lanes<U>;
+    constexpr int D1 = Core::D1, D2 = Core::D2, NW = MF::NW, ROWS = MF::ROWS;
+    constexpr int T = U > kWave ? 4 : 8;      // slabs per tile (32 or 64 KB; 8 at U = 128 would spill)
+    constexpr int RS = D1 + 4;                // padded LDS row stride (floats)
+    constexpr int R4 = D1 / 4;                // float4 per row
+    constexpr int SF4 = TileShape<D1>::SF4;   // float4 per slab
+    constexpr int TF4 = T * SF4;              // float4 per tile
+    constexpr int NT = NW * kWave;
+    constexpr int PER = (TF4 + NT - 1) / NT;  // float4 per thread and tile
+    static_assert(D1 % 4 == 0 && D1 == NW * ROWS, "rows of whole float4, split evenly over the waves");
+    __shared__ float4 xs4[T * kWave * RS / 4], os4[T * kWave * RS / 4];
+    float *xs = reinterpret_cast<float *>(xs4), *os = reinterpret_cast<float *>(os4);
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int64_t n = blockIdx.x;
+    const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+    const int64_t n_slabs = Slabs<U>::count(e1 - e0);
+    // float4 f of a tile starting at slab s0: its HBM index, or -1 past the segment
+    auto src = [&](int64_t s0, int f, int t) -> int64_t {
+      const int sl = f / SF4, in = f % SF4;
+      if (s0 + sl >= n_slabs) return -1;
+      if constexpr (U <= kWave) {
+        const int64_t base = Slabs<U>::first_edge(e0, s0) * (U * D1 / 4), end = e1 * (U * D1 / 4);
+        const int64_t g = base + f;
+        return g < end ? g : -1;
+      } else {
+        return ((e0 + s0 + sl) * U + t * kWave) * D1 / 4 + in;
+      }
+    };
+  #pragma unroll 1
+    for (int t = 0; t < L::CPL; ++t) {
+      const int u = lane % L::LPE + t * kWave;
+      float4 v[PER];
+      auto fetch = [&](int64_t s0) {
+        const float4 *x4 = reinterpret_cast<const float4 *>(x);
+  #pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const int f = tid + NT * i;
+          const int64_t g = f < TF4 ? src(s0, f, t) : -1;
+          v[i] = g >= 0 ? load_stream(x4 + g) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      };
+      // M first: its weight loads would otherwise wait behind the tile's loads
+      // (one in-order counter covers both)
+      float m[MF::MAXM];
+      {
+        CachedWeights wr;
+        wr.load(path_w, U, u);
+        float er[D2];
+        load_row<D2>(env + (n * U + u) * D2, er);
+        MF::build(wave, er, wr, m);
+      }
+      if (n_slabs > 0) fetch(0);
+      for (int64_t s0 = 0; s0 < n_slabs; s0 += T) {
+        // the tile from registers into LDS (padded rows), then the next tile's loads
+  #pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const int f = tid + NT * i;
+          if (f < TF4) *reinterpret_cast<float4 *>(xs + (f / R4) * RS + 4 * (f % R4)) = v[i];
+        }
+        if (s0 + T < n_slabs) fetch(s0 + T);
+        lds_sync<NW>();
+        const int cnt = int(n_slabs - s0 < T ? n_slabs - s0 : T);
+  #pragma unroll 1
+        for (int sl = 0; sl < cnt; ++sl) {
+          const int r = sl * kWave + lane;
+          float xr[D1], o[ROWS];
+  #pragma unroll
+          for (int q = 0; q < R4; ++q) {
+            const float4 a = *reinterpret_cast<const float4 *>(xs + r * RS + 4 * q);
+            xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
+          }
+          MF::apply(wave, xr, m, o);
+  #pragma unroll
+          for (int k = 0; k < ROWS; ++k) os[r * RS + wave * ROWS + k] = o[k];
+        }
+        lds_sync<NW>();
+        float4 *o4 = reinterpret_cast<float4 *>(out);
+  #pragma unroll
+        for (int i = 0; i < PER; ++i) {
+          const int f = tid + NT * i;
+          const int64_t g = f < TF4 ? src(s0, f, t) : -1;
+          if (g >= 0) store_stream(*reinterpret_cast<const float4 *>(os + (f / R4) * RS + 4 * (f % R4)), o4 + g);
+        }
+        // the next iteration writes xs (read above, before the barrier) and then os
+        // only after its own barrier, by which every thread has read os here
+      }
+      lds_sync<NW>();  // both tiles are free before the next channel half
+    }
   }
 }
 
@@ -833,7 +976,6 @@ __device__ __forceinline__ int swz32(int e, int k) {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void *p, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), short(0), int(bytes), 0x00020000);
 }
-constexpr int kNonTemporal = 2;
 __device__ __forceinline__ f32x4 load_tile_f4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, int(off), 0, kNonTemporal));
 }
