@@ -390,7 +390,7 @@ constexpr int kNonTemporal = 2;
 template <class Core>
 constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 
-// The per-center matrix forward at U = 128, d1 = 32, with the tiles brought
+// The per-center matrix forward at U = 64 and 128, d1 = 32, with the tiles brought
 // into LDS by direct buffer-to-LDS loads instead of through registers: the
 // registers the kernel leaves free hold one 32 KB tile, and at one workgroup
 // per compute unit one tile in flight leaves HBM latency-bound.  Four tile
@@ -420,7 +420,7 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
   constexpr int NT = NW * kWave;
   constexpr int PER = TF4 / NT;              // loads (and stores) per thread and tile
   constexpr uint32_t EDGE_BYTES = U * D1 * 4;
-  static_assert(D1 == 32 && U > kWave && TF4 % NT == 0 && D1 == NW * ROWS && ROWS == 4, "layout");
+  static_assert(D1 == 32 && U % kWave == 0 && TF4 % NT == 0 && D1 == NW * ROWS && ROWS == 4, "layout");
   __shared__ float4 xb4[NB * TF4];
   __shared__ float4 os4[TF4];  // the result tile, laid out as the tile buffers
   const uint32_t xb_lds = uint32_t(reinterpret_cast<uintptr_t>((lds_void *)xb4));
@@ -526,7 +526,7 @@ template <class Core, int U, class MF>
 __global__ __launch_bounds__(kMFwdThreads<Core>) __attribute__((amdgpu_waves_per_eu(2))) void tp_matrix_kernel(
     const int64_t *__restrict__ row_ptr, const float *__restrict__ x, const float *__restrict__ env,
     const float *__restrict__ path_w, float *__restrict__ out) {
-  if constexpr (U > kWave && Core::D1 == 32) {
+  if constexpr (U % kWave == 0 && Core::D1 == 32) {
     matrix_fwd_dma<Core, U, MF>(row_ptr, x, env, path_w, out);
   } else {
     using L = Lanes<U>;
