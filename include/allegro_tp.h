@@ -138,7 +138,9 @@ int allegro_tp_backward(const allegro_tp_plan *plan, int64_t N, int64_t E, const
                         void *stream);
 
 /* Bytes of device workspace that allegro_tp_backward_train needs for N centers:
- * (N + 128) * n_paths * U floats.  Host-only; no GPU needed. */
+ * (N + 128) * n_paths * U floats at lmax < 3; at lmax 3 max(1, min(N, 1024)) *
+ * n_paths * U floats (a bound on the matrix-core kernel's per-wave rows that
+ * holds on any device).  Host-only; no GPU needed. */
 int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t *bytes);
 
 /* Training backward: everything allegro_tp_backward computes, plus the
@@ -146,10 +148,16 @@ int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t
  * training kernels to future work, §II.D):
  *   grad_path_w[p][u] = sum_e sum_{(i,j,k) in p} C_ijk x[e,u,i] env[c(e),u,j] grad_out[e,u,k]
  * (for one scalar weight per path, sum grad_path_w over u).  The sum is
- * deterministic: each center's contribution is summed over its edges in a
- * fixed order and written to one workspace row of n_paths * U floats per
- * center (path-major, or channel-major at lmax 3), which two reduction
- * launches then sum in a fixed order.  The other four gradients
+ * deterministic.  At lmax < 3 each center's contribution is summed over its
+ * edges in a fixed order and written to one workspace row of n_paths * U
+ * floats per center (path-major), which two reduction launches then sum in a
+ * fixed order.  At lmax 3 each wave of the matrix-core kernel keeps one
+ * channel group and sums the contributions of the centers it visits, in
+ * order, into one channel-major workspace row of its own (R rounds of U rows
+ * of n_paths floats, R = its wave count over U / channels per wave: 16 on a
+ * 256-compute-unit MI355X at U = 128); one launch sums the R rounds in order.
+ * The grid is fixed per device, so the result is bit-identical run to run on
+ * one device.  The other four gradients
  * equal allegro_tp_backward's up to fp32 rounding (the two split the work
  * differently; at lmax 3 this call forms grad_x = M^T grad_out with the
  * per-center matrix of the forward).  workspace is caller-owned device memory of at least
@@ -177,14 +185,16 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
  * allegro_tp_backward_train, with the path-weight partial sums kept in a
  * static device array of the library instead of a workspace.  The array is
  * 64 MiB of fp32 (16 Mi floats) and is held by every GPU the library runs on
- * until the process ends.  The centers are processed in chunks of
- * C = floor(16 Mi / (n_paths * U)) - 384 centers (1,543 at lmax 3, U = 128;
- * 8,354 at lmax 2, U = 64); each chunk's per-center rows are summed in a fixed
- * order into one row, and the chunk rows in order into grad_path_w, so the
- * result is deterministic and equals allegro_tp_backward_train's up to fp32
- * rounding order (grad_x, grad_env, grad_w and grad_Y are bit-identical to
- * it).  At most 256 chunks: N > 256 * C returns ALLEGRO_E_INVALID before any
- * launch.  Every call on one GPU shares that GPU's array and overwrites it, so
+ * until the process ends.  At lmax 3 the matrix-core kernel's per-wave rows
+ * (at most 1024 x U x n_paths floats) fit it at any N: one launch and the
+ * same reduction as allegro_tp_backward_train, whose outputs it reproduces
+ * bit for bit.  At lmax < 3 the centers are processed in chunks of
+ * C = floor(16 Mi / (n_paths * U)) - 384 centers (8,354 at lmax 2, U = 64);
+ * each chunk's per-center rows are summed in a fixed order into one row, and
+ * the chunk rows in order into grad_path_w, so the result is deterministic and
+ * equals allegro_tp_backward_train's up to fp32 rounding order (grad_x,
+ * grad_env, grad_w and grad_Y are bit-identical to it); at most 256 chunks:
+ * N > 256 * C returns ALLEGRO_E_INVALID before any launch.  Every call on one GPU shares that GPU's array and overwrites it, so
  * calls that overlap on one GPU (several streams or threads) race and must be
  * serialised by the caller.  The call itself allocates nothing (no hipMalloc,
  * hipFree or allocating library routine); the first call on a device looks the

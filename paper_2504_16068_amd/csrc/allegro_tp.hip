@@ -906,9 +906,9 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 //     the row reads of the grad_x operand and the column reads of the G
 //     operands are conflict-free), and runs the matrix-core products;
 //   * the helper builds the next pair's M and contracts the previous pair's G
-//     (grad_env and the path-weight rows) from the generated lane tables,
-//     while its streaming wave keeps streaming; it also writes the zero sums of
-//     pairs without edges.  The helper's work is mostly LDS reads, and the
+//     (grad_env, and the path-weight sums it adds up over its pairs) from the
+//     generated lane tables, while its streaming wave keeps streaming; it also
+//     writes the zero grad_env rows of pairs without edges.  The helper's work is mostly LDS reads, and the
 //     LDS is what it shares with the streaming waves: so it keeps the terms
 //     of M it uses most (the first two of each cell) and its H indices in
 //     registers (10-bit indices, three to a word), issues the loads of the
@@ -925,8 +925,13 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
 // instructions for every tile: either would make the compiler wait for all of
 // its loads in flight at every tile.  There is no barrier between waves after
 // the tables are loaded.
-// Every sum has a fixed order.  The embedding VJP, which needs all channels
-// of grad_env[n], is embedding_vjp_kernel, launched after this kernel.
+// The grid is a multiple of U / CPW streaming waves, so every pair a wave
+// visits has the same channels: its path-weight sums stay in its helper's LDS
+// and leave as one row at the end (a few rows per channel group in all, where
+// per-center rows would be hundreds of MB), summed over the waves by
+// pw_reduce_waves_kernel.  Every sum has a fixed order.  The embedding VJP,
+// which needs all channels of grad_env[n], is embedding_vjp_kernel, launched
+// after this kernel.
 constexpr int kMfmaEdges = 16;  // edges per tile
 
 template <bool FULL>
@@ -943,8 +948,10 @@ struct MfmaShape {
   static constexpr int NW = 8, THREADS = 2 * kWave * NW;  // streaming waves, then their helpers
   static constexpr int MB = CPW * S * kWave;     // floats of a pair's M (or G) in lane layout
   static constexpr int HZ = ((Tab::NZ + 2 > Tab::RZ * kWave ? Tab::NZ + 2 : Tab::RZ * kWave) + 3) / 4 * 4;
-  // per streaming wave: tile area, M buffer, G buffer; per helper: Z / H scratch
-  static constexpr int AREA = 2 * TILE + 2 * MB, HAREA = HZ;
+  // per streaming wave: tile area, M buffer, G buffer; per helper: Z / H
+  // scratch, then its path-weight sums (CPW x RPW x 64)
+  static constexpr int PWA = CPW * Tab::RPW * kWave;
+  static constexpr int AREA = 2 * TILE + 2 * MB, HAREA = HZ + PWA;
   static_assert(NP <= 2 * kWave && Tab::WORDS % 4 == 0 && RF4 * LR == kWave && CPW * D1 == ROW, "layout");
   static constexpr int LDS_FLOATS = Tab::WORDS + NW * AREA + NW * HAREA;
   // float offset of slot group q (slots 4 q .. 4 q + 3) of lane l in a spill of
@@ -1173,7 +1180,31 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
         }
       }
     };
-    // contraction of the pair's G (in the G buffer): H, grad_env, path-weight rows
+    // The wave's path-weight gradient sums over its pairs, in pair order.  The
+    // grid holds a multiple of U / CPW streaming waves, so that a wave's pairs
+    // (every total-th) share one channel group; each wave writes one row of
+    // CPW x n_paths sums at the end, and a fixed-order sum over the waves of a
+    // channel group gives grad_path_w.
+    // The sums live in LDS (lane-owned entries, no barrier needed).
+    float *pwa = Hz + Sh::HZ;
+    auto pwa_at = [&](int cw, int r) -> float & { return pwa[(cw * Tab::RPW + r) * kWave + lane]; };
+    if constexpr (WG) {
+#pragma unroll
+      for (int cw = 0; cw < CPW; ++cw)
+#pragma unroll
+        for (int r = 0; r < Tab::RPW; ++r) pwa_at(cw, r) = 0.0f;
+    }
+    auto put_pw = [&]() {
+      if constexpr (WG) {
+        const int64_t row = (int64_t(blockIdx.x) * NW + w) * CPW;
+#pragma unroll
+        for (int cw = 0; cw < CPW; ++cw)
+#pragma unroll
+          for (int r = 0; r < Tab::RPW; ++r)
+            if (kWave * r + lane < NP) pw_part[(row + cw) * NP + kWave * r + lane] = pwa_at(cw, r);
+      }
+    };
+    // contraction of the pair's G (in the G buffer): H, grad_env, path-weight sums
     auto contract_g = [&](int64_t n, int u0) {
 #pragma unroll
       for (int cw = 0; cw < CPW; ++cw) {
@@ -1219,7 +1250,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
               const float e = __shfl(qev[cw], int(zp >> 16));
               a = __builtin_fmaf(in ? Hz[off + k] : 0.0f, e, a);
             }
-            if (p < NP) pw_part[(n * U + u) * NP + p] = a;  // channel-major row: one contiguous store
+            pwa_at(cw, r) += a;  // the wave's pairs all have channel u
           }
         }
       }
@@ -1227,9 +1258,6 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     // pairs without edges have zero sums: written here, no tiles
     auto on_empty = [&](int64_t n, int u0) {
       if (lane < CPW * D2) grad_env[(n * U + u0) * D2 + lane] = 0.0f;
-      if constexpr (WG) {
-        for (int i = lane; i < NP * CPW; i += kWave) pw_part[(n * U + u0) * NP + i] = 0.0f;
-      }
     };
     int64_t prev_n = 0;
     int prev_u0 = 0;
@@ -1251,13 +1279,19 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
     while (have) {
       const int64_t cn = walk.n;
       const int cu0 = walk.u0;
-      if (!wait_for(&hv.m_taken, k - 1, &stop, wcfg)) return;  // the wave has taken the previous M
+      if (!wait_for(&hv.m_taken, k - 1, &stop, wcfg)) {  // the wave has taken the previous M
+        put_pw();
+        return;
+      }
       build_m();
       post(&hv.m_ready, k);
       have = walk.next(row_ptr, on_empty);
       if (have) load_params(walk.n, walk.u0);
       if (k > 0) {
-        if (!wait_for(&hv.g_written, k - 1, &stop, wcfg)) return;
+        if (!wait_for(&hv.g_written, k - 1, &stop, wcfg)) {
+          put_pw();
+          return;
+        }
         contract_g(prev_n, prev_u0);
         post(&hv.g_taken, k - 1);
       }
@@ -1270,6 +1304,7 @@ __global__ __launch_bounds__(MfmaShape<FULL>::THREADS) void tp_mfma_bwd_kernel(
       contract_g(prev_n, prev_u0);
       post(&hv.g_taken, k - 1);
     }
+    put_pw();
     return;
   }
 
@@ -1579,15 +1614,25 @@ __global__ __launch_bounds__(256) void pw_reduce_rows_kernel(int64_t N, int cols
   chunk_sums[int64_t(blockIdx.y) * cols + c] = (a0 + a1) + (a2 + a3);
 }
 
-// With np > 0 the rows are channel-major ([U][np], column c = u np + p) and
-// the sum goes to grad_pw[p][u]; with np == 0 columns map one to one.
 __global__ __launch_bounds__(256) void pw_reduce_chunks_kernel(int rows, int cols, const float *__restrict__ chunk_sums,
-                                                               float *__restrict__ grad_pw, int np) {
+                                                               float *__restrict__ grad_pw) {
   const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
   if (c >= cols) return;
   float a = 0.0f;
   for (int r = 0; r < rows; ++r) a += chunk_sums[int64_t(r) * cols + c];
-  grad_pw[np > 0 ? (c % np) * (cols / np) + c / np : c] = a;
+  grad_pw[c] = a;
+}
+
+// The matrix-core backward's path-weight rows: part[R][U][np], one row per
+// streaming wave; grad_pw[p][u] is the sum over r of part[r][u][p], in order.
+__global__ __launch_bounds__(256) void pw_reduce_waves_kernel(int R, int U, int np, const float *__restrict__ part,
+                                                              float *__restrict__ grad_pw) {
+  const int c = int(blockIdx.x) * 256 + int(threadIdx.x);
+  if (c >= U * np) return;
+  const int p = c / U, u = c % U;
+  float a = 0.0f;
+  for (int r = 0; r < R; ++r) a += part[(int64_t(r) * U + u) * np + p];
+  grad_pw[c] = a;
 }
 
 __global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restrict__ p) {
@@ -1601,6 +1646,7 @@ __global__ __launch_bounds__(256) void zero_floats_kernel(int n, float *__restri
 // (64 MiB), held by every GPU the library runs on until the process ends.
 constexpr int64_t kNoAllocFloats = int64_t(16) << 20;
 constexpr int64_t kNoAllocChunks = 256;  // chunk rows kept for the last sum
+constexpr int kMaxPwRounds = 1024;        // per-wave row rounds of the matrix-core backward
 static __device__ __align__(256) float scratch[kNoAllocFloats];
 
 // ------------------------------------------------------------- host side
@@ -1685,9 +1731,22 @@ unsigned mfma_grid(int64_t N) {
     }
     res = resident[dev];
   }
-  const int64_t pairs = N * (U / MfmaShape<FULL>::CPW);
-  const int64_t blocks = (pairs + MfmaShape<FULL>::NW - 1) / MfmaShape<FULL>::NW;
-  return unsigned(blocks < res ? blocks : res);
+  // a multiple of GB workgroups, so that the streaming waves number a
+  // multiple of the channel groups (each wave keeps one group)
+  constexpr int GROUPS = U / MfmaShape<FULL>::CPW, GB = GROUPS / MfmaShape<FULL>::NW;
+  static_assert(GROUPS % MfmaShape<FULL>::NW == 0, "whole channel groups per round of waves");
+  const int64_t blocks = N * GB;  // one streaming wave per pair
+  int64_t cap = res >= GB ? res / GB * GB : GB;
+  if (cap > int64_t(kMaxPwRounds) * GB) cap = int64_t(kMaxPwRounds) * GB;
+  return unsigned(blocks < cap ? blocks : cap);
+}
+
+// Rows of U x n_paths path-weight sums the matrix-core backward writes for N
+// centers: one per round of streaming waves over the channel groups, at most
+// min(N, kMaxPwRounds) on any device.
+template <bool FULL, int U>
+int64_t mfma_pw_rounds(int64_t N) {
+  return int64_t(mfma_grid<FULL, U, true>(N)) * MfmaShape<FULL>::NW / (U / MfmaShape<FULL>::CPW);
 }
 
 template <class Core, int U, bool WG>
@@ -1695,8 +1754,8 @@ void launch_bwd(dim3 grid, hipStream_t s, const int64_t *rp, const float *x, con
                 const float *g, const float *w, const float *Y, float *gx, float *genv, float *gw, float *gy,
                 float *pw_part, WaitCfg wcfg) {
   if constexpr (Core::LMAX >= 3 && WG) {
-    // training backward at lmax 3: grad_x, grad_env and the path-weight rows on
-    // the matrix cores (one read of x and g), then the embedding VJP from the
+    // training backward at lmax 3: grad_x, grad_env and per-wave path-weight
+    // sums on the matrix cores (one read of x and g), then the embedding VJP from the
     // complete grad_env.  The inference backward stays on the direct kernel,
     // which is faster there (10.3 against 12.0 ms on 20,000 centers, U = 128).
     const int64_t N = grid.x;
@@ -1713,7 +1772,10 @@ struct Kernels {
   EnvFn env = nullptr;
   FwdFn fwd = nullptr;
   BwdFn bwd = nullptr;
-  BwdFn bwd_wg = nullptr;  // also writes the per-center path-weight gradient
+  BwdFn bwd_wg = nullptr;  // also writes path-weight gradient partial sums
+  // matrix-core training backward: rounds of per-wave path-weight rows it
+  // writes for N centers (null for the direct kernels' per-center rows)
+  int64_t (*pw_rounds)(int64_t N) = nullptr;
 };
 
 template <int LMAX, bool FULL, int U>
@@ -1724,6 +1786,7 @@ Kernels kernels_for(bool det) {
   k.fwd = &launch_fwd<Core, U>;
   k.bwd = &launch_bwd<Core, U, false>;
   k.bwd_wg = &launch_bwd<Core, U, true>;
+  if constexpr (LMAX >= 3) k.pw_rounds = &mfma_pw_rounds<FULL, U>;
   return k;
 }
 
@@ -1970,15 +2033,15 @@ int allegro_tp_backward_workspace(const allegro_tp_plan *plan, int64_t N, size_t
   if (N < 0 || N >= (int64_t(1) << 31)) return fail(ALLEGRO_E_INVALID, "N=%lld out of range", (long long)N);
   if (!bytes) return fail(ALLEGRO_E_INVALID, "bytes is NULL");
   const int64_t cols = int64_t(plan->table.paths.size()) * plan->U;
-  *bytes = size_t((N + kPwChunks) * cols) * sizeof(float);
+  // the matrix-core kernel's per-wave rows (one per round of its waves over
+  // the channel groups: at most one per center and at most kMaxPwRounds; a
+  // bound that needs no device query), else one row per center and the range
+  // sums
+  const int64_t rows = select(plan).pw_rounds ? std::max<int64_t>(std::min<int64_t>(N, kMaxPwRounds), 1)
+                                              : N + kPwChunks;
+  *bytes = size_t(rows * cols) * sizeof(float);
   return ALLEGRO_OK;
 }
-
-// Layout of the per-center path-weight rows the training backward writes:
-// [n_paths][U] (returns 0) from the direct kernels, channel-major [U][n_paths]
-// (returns n_paths) from the matrix-core kernel at lmax 3, where a channel's
-// row is one contiguous store.
-static int pw_rows_np(const allegro_tp_plan *plan) { return plan->lmax >= 3 ? int(plan->table.paths.size()) : 0; }
 
 int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E, const int64_t *row_ptr,
                               const float *x, const float *env, const float *path_w, const float *grad_out,
@@ -2018,14 +2081,18 @@ int allegro_tp_backward_train(const allegro_tp_plan *plan, int64_t N, int64_t E,
   const Kernels k = select(plan);
   if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
   float *part = static_cast<float *>(workspace);
-  float *chunks = part + N * cols;
   k.bwd_wg(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, part,
            WaitCfg{plan->spin_limit, validate ? plan->status : nullptr});
   if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
   const unsigned cb = unsigned((cols + 255) / 256);
-  hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
-  hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w,
-                     pw_rows_np(plan));
+  if (k.pw_rounds) {
+    hipLaunchKernelGGL(pw_reduce_waves_kernel, dim3(cb), dim3(256), 0, s, int(k.pw_rounds(N)), plan->U,
+                       int(plan->table.paths.size()), part, grad_path_w);
+  } else {
+    float *chunks = part + N * cols;
+    hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, N, cols, part, chunks);
+    hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, chunks, grad_path_w);
+  }
   if ((rc = after_launch("allegro_tp_backward_train"))) return rc;
   return validate ? check_handover_locked(mp, s, "allegro_tp_backward_train") : ALLEGRO_OK;
 }
@@ -2043,9 +2110,11 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
     hipLaunchKernelGGL(zero_floats_kernel, dim3(unsigned((cols + 255) / 256)), dim3(256), 0, s, cols, grad_path_w);
     return after_launch("allegro_tp_backward_train_noalloc");
   }
+  const Kernels k = select(plan);
+  if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
   const NoAllocLayout lay = noalloc_layout(cols);
   const int64_t n_chunks = (N + lay.centers - 1) / lay.centers;
-  if (lay.centers < 1 || n_chunks > kNoAllocChunks)
+  if (!k.pw_rounds && (lay.centers < 1 || n_chunks > kNoAllocChunks))
     return fail(ALLEGRO_E_INVALID,
                 "N=%lld centers exceed the allocation-free maximum of %lld for this plan (%d path-weight columns, "
                 "%zu-byte static scratch)", (long long)N, (long long)lay.centers * kNoAllocChunks, cols,
@@ -2067,13 +2136,22 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
     if ((rc = validate_csr_locked(mp, N, E, row_ptr, s))) return rc;
   }
   const WaitCfg wcfg{plan->spin_limit, validate ? plan->status : nullptr};
-  const Kernels k = select(plan);
-  if (!k.bwd_wg) return fail(ALLEGRO_E_UNSUPPORTED, "no kernel for this plan");
+  const unsigned cb = unsigned((cols + 255) / 256);
+  if (k.pw_rounds) {
+    // the matrix-core kernel's per-wave rows fit the scratch at any N
+    static_assert(kNoAllocFloats >= int64_t(kMaxPwRounds) * 128 * 68, "per-wave rows fit the scratch");
+    const int64_t rounds = k.pw_rounds(N);  // at most kMaxPwRounds
+    k.bwd_wg(dim3(unsigned(N)), s, row_ptr, x, env, path_w, grad_out, w, Y, grad_x, grad_env, grad_w, grad_Y, scr,
+             wcfg);
+    hipLaunchKernelGGL(pw_reduce_waves_kernel, dim3(cb), dim3(256), 0, s, int(rounds), plan->U,
+                       int(plan->table.paths.size()), scr, grad_path_w);
+    if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
+    return validate ? check_handover_locked(mp, s, "allegro_tp_backward_train_noalloc") : ALLEGRO_OK;
+  }
   // scratch: per-center rows of one chunk, the 128 range sums of a chunk, then
   // one row per chunk; every region is fully written before it is read
   float *part = scr, *ranges = part + lay.centers * cols, *chunk_rows = ranges + int64_t(kPwChunks) * cols;
   const int64_t ud2 = int64_t(plan->U) * plan->table.d2;
-  const unsigned cb = unsigned((cols + 255) / 256);
   for (int64_t c = 0; c < n_chunks; ++c) {
     const int64_t n0 = c * lay.centers, n1 = std::min(N, n0 + lay.centers);
     // the chunk's centers as a CSR of their own: row_ptr values stay absolute
@@ -2082,11 +2160,11 @@ int allegro_tp_backward_train_noalloc(const allegro_tp_plan *plan, int64_t N, in
              grad_env + n0 * ud2, grad_w, grad_Y, part, wcfg);
     hipLaunchKernelGGL(pw_reduce_rows_kernel, dim3(cb, kPwChunks), dim3(256), 0, s, n1 - n0, cols, part, ranges);
     hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, kPwChunks, cols, ranges,
-                       chunk_rows + c * cols, 0);
+                       chunk_rows + c * cols);
     if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
   }
   hipLaunchKernelGGL(pw_reduce_chunks_kernel, dim3(cb), dim3(256), 0, s, int(n_chunks), cols, chunk_rows,
-                     grad_path_w, pw_rows_np(plan));
+                     grad_path_w);
   if ((rc = after_launch("allegro_tp_backward_train_noalloc"))) return rc;
   return validate ? check_handover_locked(mp, s, "allegro_tp_backward_train_noalloc") : ALLEGRO_OK;
 }

@@ -51,9 +51,15 @@ int main(void) {
         CHECK(norm[p * d1 + k] == 0.0 || (norm[p * d1 + k] > 1 - 1e-12 && norm[p * d1 + k] < 1 + 1e-12),
               "normalisation path %d component %d: %.17g", p, k, norm[p * d1 + k]);
     size_t bytes = 0;
+    /* per-center rows and 128 range sums, or at lmax 3 at most one per-wave row
+     * round per center (at most 1024 rounds) */
+    const size_t rows = lmax >= 3 ? 1000 : 1000 + 128;
     CHECK(allegro_tp_backward_workspace(plan, 1000, &bytes) == ALLEGRO_OK &&
-              bytes == (size_t)(1000 + 128) * (size_t)np * 64 * sizeof(float),
+              bytes == rows * (size_t)np * 64 * sizeof(float),
           "workspace size %zu", bytes);
+    CHECK(lmax < 3 || (allegro_tp_backward_workspace(plan, 5000, &bytes) == ALLEGRO_OK &&
+                       bytes == (size_t)1024 * (size_t)np * 64 * sizeof(float)),
+          "workspace size %zu at N=5000", bytes);
     /* rejected before any GPU call */
     CHECK(allegro_tp_forward(plan, -1, 0, NULL, NULL, NULL, NULL, NULL, NULL) == ALLEGRO_E_INVALID, "N<0");
     CHECK(strstr(allegro_last_error(), "negative") != NULL, "message");

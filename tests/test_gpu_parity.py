@@ -390,9 +390,10 @@ def test_sh_headline_vectors_sampled(at):
 
 def _train(at, plan, rp, x, env, pw, g, w, y):
     """The training backward into outputs filled with NaN, so that an element the
-    kernels leave unwritten fails every comparison."""
+    kernels leave unwritten fails every comparison (the workspace too: rows it
+    does not write stay NaN)."""
     n = rp.numel() - 1
-    ws = torch.empty(at.allegro_tp_backward_workspace(plan, n), dtype=torch.uint8, device=DEV)
+    ws = torch.full((at.allegro_tp_backward_workspace(plan, n) // 4,), float("nan"), device=DEV).view(torch.uint8)
     outs = tuple(torch.full_like(a, float("nan")) for a in (x, env, w, y, pw))
     res = at.allegro_tp_backward_train(plan, rp, x, env, pw, g, w, y, outs=outs, workspace=ws)
     torch.cuda.synchronize()
@@ -501,8 +502,13 @@ def test_train_backward_rejects_small_workspace(at):
 
 @pytest.mark.parametrize("name", ["headline", "high_order", "large"])
 def test_train_backward_full_size(at, name, n_samples=16):
-    """Per-center partial sums (the workspace's first N * P * U floats) on sampled
-    centers against the oracle; the reduction against the fp64 sum of all rows."""
+    """Full size, sampled: grad_x and each sampled center's path-weight rows
+    against the oracle, and grad_path_w against the fp64 sum of the partial rows
+    the workspace holds.  At lmax < 3 those are per-center rows ([N][P][U]); at
+    lmax 3 the matrix-core kernel writes one [U][P] row per round of its waves
+    (each the sum over the centers that round visited), so a center's own row is
+    taken from a second call on a one-center CSR that points into the same
+    tensors (its grad_path_w is that row)."""
     graph = workloads.make_graph(name)
     cfg = graph.config
     _note(f"[gpu] training backward {name}: N={graph.n_atoms} E={graph.n_edges} (sampled)")
@@ -515,14 +521,21 @@ def test_train_backward_full_size(at, name, n_samples=16):
     # every element written (the outputs start as NaN)
     for name_, a in (("grad_x", gx), ("grad_env", genv), ("grad_w", gw), ("grad_Y", gy), ("grad_path_w", gpw)):
         assert not bool(torch.isnan(a).any()), f"{name_} has unwritten elements"
-    del genv, gw, gy
     n, cols = graph.n_atoms, plan.n_paths * cfg.U
-    rows = ws[: n * cols * 4].view(torch.float32)
-    # a center's row is path-major [P][U], or channel-major [U][P] at lmax 3
+    wsf = ws.view(torch.float32)
     if cfg.lmax >= 3:
-        part = rows.view(n, cfg.U, plan.n_paths).permute(0, 2, 1)
+        # rows written: a prefix of whole [U][P] rows, the rest still NaN
+        rows = wsf.view(-1, cfg.U, plan.n_paths)
+        written = ~torch.isnan(rows).view(rows.shape[0], -1).any(dim=1)
+        n_rows = int(written.sum())
+        assert n_rows >= 1 and bool(written[:n_rows].all()) and not bool(written[n_rows:].any())
+        part = rows[:n_rows].permute(0, 2, 1)
     else:
-        part = rows.view(n, plan.n_paths, cfg.U)
+        n_rows = n
+        part = wsf[: n * cols].view(n, plan.n_paths, cfg.U)
+    ph = np.ascontiguousarray(part.cpu().numpy()).astype(np.float64).reshape(n_rows, cols)
+    del part, ws, wsf
+    ws1 = torch.empty(at.allegro_tp_backward_workspace(plan, 1), dtype=torch.uint8, device=DEV)
     rng = np.random.default_rng(cfg.index + 50)
     centers = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, n_samples)]))
     t = otp.TensorProduct(cfg.lmax, cfg.full_parity)
@@ -532,14 +545,29 @@ def test_train_backward_full_size(at, name, n_samples=16):
         local = np.array([0, e - s], np.int64)
         env_c = otp.env_embed(local, ws_, graph.Y[s:e])
         ref = t.path_weight_grad(local, xs, env_c, gs)
-        assert block_rel_err(part[c].cpu().numpy(), ref) <= BWD_TOL, c
+        if cfg.lmax >= 3:
+            before = [a[s:e].clone() for a in (gx, gw, gy)]
+            o_env = torch.full_like(genv[c:c + 1], float("nan"))
+            o_pw = torch.full_like(gpw, float("nan"))
+            at.allegro_tp_backward_train(plan, rp[c:c + 2], x, env[c:c + 1], pwd, g, w, yd,
+                                         outs=(gx, o_env, gw, gy, o_pw), workspace=ws1)
+            torch.cuda.synchronize()
+            for a, b in zip((gx, gw, gy), before):
+                assert _same_bits(a[s:e], b), c  # the same rows as in the full call
+            assert _same_bits(o_env[0], genv[c]), c
+            row = o_pw.cpu().numpy()
+        else:
+            row = ph[c].reshape(plan.n_paths, cfg.U)
+        assert block_rel_err(row, ref) <= BWD_TOL, c
         ref_gx = t.backward(local, xs, env_c, pw, gs, ws_, graph.Y[s:e])[0]
         assert block_rel_err(gx[s:e].cpu().numpy(), ref_gx, t.x_slices) <= BWD_TOL, c
-    del gx
-    ph = np.ascontiguousarray(part.cpu().numpy()).astype(np.float64).reshape(n, cols)
+    del gx, genv, gw, gy
     total = ph.sum(axis=0)
-    # recursive-summation bound: at most ceil(ceil(N / 128) / 4) + 130 sequential fp32 additions
-    depth = -(-(-(-n // 128)) // 4) + 130
+    if cfg.lmax >= 3:
+        depth = n_rows + 1  # one fixed-order sum over the rows
+    else:
+        # recursive-summation bound: at most ceil(ceil(N / 128) / 4) + 130 sequential fp32 additions
+        depth = -(-(-(-n // 128)) // 4) + 130
     bound = 1.01 * depth * 2.0 ** -24 * np.abs(ph).sum(axis=0)
     got = gpw.cpu().numpy().reshape(cols).astype(np.float64)
     assert np.all(np.abs(got - total) <= bound)
