@@ -92,12 +92,12 @@ def algorithmic_bytes(cfg, n_atoms: int, n_edges: int):
 
 def mfma_bwd_bytes(cfg, n_atoms: int, n_edges: int):
     """Algorithmic bytes of the lmax-3 training backward's first kernel (tp_mfma_bwd_kernel):
-    read x, g [E,U,d1] and env; write grad_x [E,U,d1], grad_env [N,U,d2] and the
-    per-center path-weight rows [N,P,U]."""
+    read x, g [E,U,d1] and env; write grad_x [E,U,d1] and grad_env [N,U,d2].  Its
+    path-weight partial sums (one [U][P] row per round of its waves, 16 rounds
+    on a 256-CU device: about 0.6 MB at U = 128) are left out."""
     d1, d2, n_paths = workloads.dims(cfg.lmax, cfg.full_parity)
     u = cfg.U
-    return (4 * (3 * n_edges * u * d1 + 2 * n_atoms * u * d2 + n_atoms * n_paths * u) + (n_atoms + 1) * 8
-            + n_paths * u * 4)
+    return 4 * (3 * n_edges * u * d1 + 2 * n_atoms * u * d2) + (n_atoms + 1) * 8 + n_paths * u * 4
 
 
 def kernel_source_digest() -> str:
