@@ -398,10 +398,11 @@ constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 // flight per compute unit; the four buffers and the result tile fill the
 // 160 KB of LDS).  A load lands at the LDS address of its lane, so the source
 // addresses carry the layout: row r (slab r / 64, channel r % 64) holds its
-// 16-byte chunk q at position q ^ ((r / 2) mod 8), which keeps the rows'
-// 16-byte accesses (lane r reads row r, 16 lanes at a time over the 64 banks)
-// free of bank conflicts without padding; the result tile uses the same
-// layout.  The waits for a tile's loads are explicit (the compiler does not
+// 16-byte chunk q at position q ^ s(r), s(r) = (r mod 8) ^ ((r / 8) mod 2), so
+// that the rows' 16-byte accesses (lane r reads row r) put any 8 consecutive
+// lanes on 8 distinct 16-byte columns and any 16 on distinct bank groups of a
+// 256-byte span, without padding (the profiler counts no bank conflicts); the
+// result tile uses the same layout.  The waits for a tile's loads are explicit (the compiler does not
 // track loads into LDS): every iteration issues the same number of loads and
 // stores (past the segment their descriptors have no range), so the number
 // issued after tile k's loads is fixed.
@@ -452,7 +453,7 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
         const int blk = wave * PER + i, slot = blk * kWave + lane;
-        const int r = slot / R4, q = (slot % R4) ^ ((r >> 1) & 7);
+        const int r = slot / R4, q = (slot % R4) ^ ((r & 7) ^ ((r >> 3) & 1));
         const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(q) * 16;
         asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
                      :
@@ -496,11 +497,11 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
         float xr[D1], o[ROWS];
 #pragma unroll
         for (int q = 0; q < R4; ++q) {
-          const float4 a = xb[r * R4 + (q ^ ((r >> 1) & 7))];
+          const float4 a = xb[r * R4 + (q ^ ((r & 7) ^ ((r >> 3) & 1)))];
           xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
         }
         MF::apply(wave, xr, m, o);
-        os4[r * R4 + (wave ^ ((r >> 1) & 7))] = make_float4(o[0], o[1], o[2], o[3]);
+        os4[r * R4 + (wave ^ ((r & 7) ^ ((r >> 3) & 1)))] = make_float4(o[0], o[1], o[2], o[3]);
       }
       lds_sync<NW>();
       const auto ro = tile_rsrc(out, k);
@@ -508,7 +509,7 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
       for (int i = 0; i < PER; ++i) {
         const int f = tid + NT * i, r = f / R4, c = f % R4;
         const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(c) * 16;
-        const float4 v = os4[r * R4 + (c ^ ((r >> 1) & 7))];
+        const float4 v = os4[r * R4 + (c ^ ((r & 7) ^ ((r >> 3) & 1)))];
         __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y),
                                                      __float_as_uint(v.z), __float_as_uint(v.w)},
                                                ro, int(voff), 0, kNonTemporal);
