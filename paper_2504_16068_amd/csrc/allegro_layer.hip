@@ -112,13 +112,20 @@ __device__ __forceinline__ void stage_rows(const float *__restrict__ x, int64_t 
 
 // C[E][N] = X[E][K] B[K][N] over 64-row tiles.  Wave w owns the column tiles
 // w + 4 j of every row tile and keeps their B operands in registers for the
-// whole launch; A operands come from the LDS tile.
+// whole launch; A operands come from the LDS tile.  The products of the tile
+// go back through LDS (over the X tile), so that the epilogue reads its addend
+// and writes its output as whole rows, 16 bytes per lane and consecutive
+// lanes along a row: written straight from the accumulators, each store
+// instruction would cover 64-byte pieces of four rows.
 template <int K1, int K2, int N, int N1, int PRO, int EPI>
 __global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
   constexpr int K = K1 + K2, XS = K + 4;  // row stride: the 16 rows of an A read hit distinct banks
+  constexpr int OS = N + 4;               // row stride of the product tile
   constexpr int NJ = N / 64;              // column tiles per wave
-  static_assert(K1 % 16 == 0 && K2 % 16 == 0 && N % 64 == 0 && N1 % 16 == 0, "tile shape");
-  __shared__ float4 xs4[kRowTile * XS / 4];
+  constexpr int LDSF = kRowTile * (XS > OS ? XS : OS);
+  constexpr int OF4 = kRowTile * N / 4, OPER = OF4 / kThreads;  // product float4 per thread
+  static_assert(K1 % 16 == 0 && K2 % 16 == 0 && N % 64 == 0 && N1 % 16 == 0 && OF4 % kThreads == 0, "tile shape");
+  __shared__ float4 xs4[LDSF / 4];
   float *xs = reinterpret_cast<float *>(xs4);
   const int tid = threadIdx.x, wave = tid / kWave, l = tid % kWave;
   // step s pairs k = 4 s + l / 16 in both operands
@@ -135,41 +142,65 @@ __global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
     stage_rows<K1, PRO>(g.x1, r0, rows, xs, XS, 0, tid);
     if constexpr (K2 > 0) stage_rows<K2, kProNone>(g.x2, r0, rows, xs, XS, K1, tid);
     lds_sync<4>();
-#pragma unroll 1
+    f32x4 acc[kRowTile / 16][NJ];
+#pragma unroll
     for (int rt = 0; rt < kRowTile / 16; ++rt) {
       // with XS = 4 (mod 64) the 64 lanes of an A read hit distinct banks
       const float *xa = xs + (16 * rt + l % 16) * XS + l / 16;
-      f32x4 acc[NJ];
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < NJ; ++j) acc[rt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < K / 4; ++s) {
         const float a = xa[4 * s];
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) acc[j] = mfma_16x16x4(a, bf[j][s], acc[j]);
+        for (int j = 0; j < NJ; ++j) acc[rt][j] = mfma_16x16x4(a, bf[j][s], acc[rt][j]);
       }
+    }
+    lds_sync<4>();  // every wave has read the X tile: its LDS takes the products
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        const int ct = wave + 4 * j, n = 16 * ct + l % 16;
+    for (int rt = 0; rt < kRowTile / 16; ++rt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int row = 16 * rt + 4 * (l / 16) + r;
-          if (row >= rows) continue;
+      for (int j = 0; j < NJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          xs[(16 * rt + 4 * (l / 16) + r) * OS + 16 * (wave + 4 * j) + l % 16] = acc[rt][j][r];
+    lds_sync<4>();
+    // epilogue by whole rows: float4 f = tid + 256 i is row f / (N / 4), columns 4 (f % (N / 4)) ..
+    float4 dv[OPER];
+    if constexpr (EPI != kEpiStore) {
+#pragma unroll
+      for (int i = 0; i < OPER; ++i) {
+        const int f = tid + kThreads * i, row = f / (N / 4), col = 4 * (f % (N / 4));
+        dv[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < rows && (EPI != kEpiSplitAdd || col < N1)) {
           const int64_t e = r0 + row;
-          if constexpr (EPI == kEpiStore) {
-            g.c[e * N + n] = acc[j][r];
-          } else if constexpr (EPI == kEpiAdd) {
-            g.c[e * N + n] = acc[j][r] + g.d[e * N + n];
-          } else if constexpr (EPI == kEpiSiluGrad) {
-            g.c[e * N + n] = acc[j][r] * silu_grad(g.d[e * N + n]);
-          } else {
-            if (16 * ct < N1) g.c[e * N1 + n] = acc[j][r] + g.d[e * N1 + n];
-            else g.c2[e * (N - N1) + (n - N1)] = acc[j][r];
-          }
+          dv[i] = *reinterpret_cast<const float4 *>(g.d + e * (EPI == kEpiSplitAdd ? N1 : N) + col);
         }
       }
     }
-    lds_sync<4>();
+#pragma unroll
+    for (int i = 0; i < OPER; ++i) {
+      const int f = tid + kThreads * i, row = f / (N / 4), col = 4 * (f % (N / 4));
+      if (row >= rows) continue;
+      const int64_t e = r0 + row;
+      float4 v = *reinterpret_cast<const float4 *>(xs + row * OS + col);
+      if constexpr (EPI == kEpiAdd) {
+        v.x += dv[i].x; v.y += dv[i].y; v.z += dv[i].z; v.w += dv[i].w;
+      } else if constexpr (EPI == kEpiSiluGrad) {
+        v.x *= silu_grad(dv[i].x); v.y *= silu_grad(dv[i].y); v.z *= silu_grad(dv[i].z); v.w *= silu_grad(dv[i].w);
+      }
+      if constexpr (EPI == kEpiSplitAdd) {
+        if (col < N1) {
+          v.x += dv[i].x; v.y += dv[i].y; v.z += dv[i].z; v.w += dv[i].w;
+          *reinterpret_cast<float4 *>(g.c + e * N1 + col) = v;
+        } else {
+          *reinterpret_cast<float4 *>(g.c2 + e * (N - N1) + (col - N1)) = v;
+        }
+      } else {
+        *reinterpret_cast<float4 *>(g.c + e * N + col) = v;
+      }
+    }
+    lds_sync<4>();  // the products are read: the next X tile may land
   }
 }
 
