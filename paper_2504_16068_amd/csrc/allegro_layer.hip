@@ -110,6 +110,35 @@ __device__ __forceinline__ void stage_rows(const float *__restrict__ x, int64_t 
   }
 }
 
+// stage_rows in two halves, so that a tile's loads can be in flight while the
+// previous tile is multiplied: the loads into registers, then the LDS writes.
+template <int KX>
+struct RowRegs {
+  static constexpr int F4 = kRowTile * KX / 4, PER = (F4 + kThreads - 1) / kThreads;
+  float4 v[PER];
+  __device__ __forceinline__ void load(const float *__restrict__ x, int64_t r0, int rows, int tid) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = tid + kThreads * i, r = f / (KX / 4), k = 4 * (f % (KX / 4));
+      v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (f < F4 && r < rows) v[i] = *reinterpret_cast<const float4 *>(x + (r0 + r) * KX + k);
+    }
+  }
+  template <int PRO>
+  __device__ __forceinline__ void put(float *xs, int XS, int col0, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int f = tid + kThreads * i, r = f / (KX / 4), k = 4 * (f % (KX / 4));
+      if (f >= F4) continue;
+      float4 u = v[i];
+      if constexpr (PRO == kProSilu) {
+        u.x = silu(u.x); u.y = silu(u.y); u.z = silu(u.z); u.w = silu(u.w);
+      }
+      *reinterpret_cast<float4 *>(xs + r * XS + col0 + k) = u;
+    }
+  }
+};
+
 // C[E][N] = X[E][K] B[K][N] over 64-row tiles.  Wave w owns the column tiles
 // w + 4 j of every row tile and keeps their B operands in registers for the
 // whole launch; A operands come from the LDS tile.  The products of the tile
@@ -224,13 +253,26 @@ __global__ __launch_bounds__(kThreads) void reduce_gemm_kernel(int64_t E, const 
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[mt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int64_t n_tiles = (E + kRedTile - 1) / kRedTile;
-  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+  static_assert(kRedTile == kRowTile, "tiles staged by RowRegs");
+  // the next tile's loads are issued before this tile's products, into the
+  // registers this tile's rows have just left
+  RowRegs<M1> r1;
+  RowRegs<(M2 > 0 ? M2 : 4)> r2;
+  RowRegs<N> rq;
+  auto load = [&](int64_t t) {
     const int64_t r0 = t * kRedTile;
     const int rows = int(E - r0 < kRedTile ? E - r0 : kRedTile);
-    stage_rows<M1, PRO>(p1, r0, rows, ps, PS, 0, tid);
-    if constexpr (M2 > 0) stage_rows<M2, kProNone>(p2, r0, rows, ps, PS, M1, tid);
-    stage_rows<N, kProNone>(q, r0, rows, qs, QS, 0, tid);
+    r1.load(p1, r0, rows, tid);
+    if constexpr (M2 > 0) r2.load(p2, r0, rows, tid);
+    rq.load(q, r0, rows, tid);
+  };
+  if (int64_t(blockIdx.x) < n_tiles) load(blockIdx.x);
+  for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+    r1.template put<PRO>(ps, PS, 0, tid);
+    if constexpr (M2 > 0) r2.template put<kProNone>(ps, PS, M1, tid);
+    rq.template put<kProNone>(qs, QS, 0, tid);
     lds_sync<4>();
+    if (t + gridDim.x < n_tiles) load(t + gridDim.x);
     // the sum runs over the tile's edges: step s pairs edge 4 s + l / 16
     const float *pa = ps + (l / 16) * PS + l % 16;
     const float *qb = qs + (l / 16) * QS + 16 * wave + l % 16;
