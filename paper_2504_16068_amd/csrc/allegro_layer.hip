@@ -165,12 +165,23 @@ __global__ __launch_bounds__(kThreads) void row_gemm_kernel(RowGemmArgs g) {
     for (int s = 0; s < K / 4; ++s)
       bf[j][s] = g.b[(4 * s + l / 16) * g.b_rs + (16 * (wave + 4 * j) + l % 16) * g.b_cs];
   const int64_t n_tiles = (g.E + kRowTile - 1) / kRowTile;
+  // the next tile's rows are loaded while this tile is multiplied
+  RowRegs<K1> x1r;
+  RowRegs<(K2 > 0 ? K2 : 4)> x2r;
+  auto load = [&](int64_t t) {
+    const int64_t r0 = t * kRowTile;
+    const int rows = int(g.E - r0 < kRowTile ? g.E - r0 : kRowTile);
+    x1r.load(g.x1, r0, rows, tid);
+    if constexpr (K2 > 0) x2r.load(g.x2, r0, rows, tid);
+  };
+  if (int64_t(blockIdx.x) < n_tiles) load(blockIdx.x);
   for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
     const int64_t r0 = t * kRowTile;
     const int rows = int(g.E - r0 < kRowTile ? g.E - r0 : kRowTile);
-    stage_rows<K1, PRO>(g.x1, r0, rows, xs, XS, 0, tid);
-    if constexpr (K2 > 0) stage_rows<K2, kProNone>(g.x2, r0, rows, xs, XS, K1, tid);
+    x1r.template put<PRO>(xs, XS, 0, tid);
+    if constexpr (K2 > 0) x2r.template put<kProNone>(xs, XS, K1, tid);
     lds_sync<4>();
+    if (t + gridDim.x < n_tiles) load(t + gridDim.x);
     f32x4 acc[kRowTile / 16][NJ];
 #pragma unroll
     for (int rt = 0; rt < kRowTile / 16; ++rt) {
