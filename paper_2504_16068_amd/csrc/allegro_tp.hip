@@ -124,18 +124,31 @@ __device__ __forceinline__ void env_accumulate(float (&acc)[Lanes<U>::CPL][D2], 
       acc[t][j] = DET ? add_rounded_product(acc[t][j], wv[t], y[j]) : __builtin_fmaf(wv[t], y[j], acc[t][j]);
 }
 
+// Waves per workgroup of the embedding: each wave takes its own center (or
+// its own G centers when U < 64).  One-wave workgroups left too few waves
+// resident per compute unit.
+constexpr int kEnvWaves = 4;
+
 template <int U, int D2, bool DET>
-__global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64_t *__restrict__ row_ptr,
-                                                          const float *__restrict__ w,
-                                                          const float *__restrict__ Y, float *__restrict__ env) {
+__global__ __launch_bounds__(kWave * kEnvWaves) void env_embed_kernel(int64_t N, const int64_t *__restrict__ row_ptr,
+                                                                      const float *__restrict__ w,
+                                                                      const float *__restrict__ Y,
+                                                                      float *__restrict__ env) {
   using L = Lanes<U>;
   constexpr int B = D2 <= 9 ? 8 : 4;  // edges whose loads are in flight together
-  const int lane = threadIdx.x, grp = lane / L::LPE, ul = lane % L::LPE;
+  constexpr int RF = kWave * L::CPL * D2;  // floats of the wave's env rows
+  static_assert(RF % 4 == 0, "whole float4 of env rows per wave");
+  __shared__ float4 rows4[kEnvWaves * RF / 4];
+  const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+  const int lane = int(threadIdx.x) % kWave, grp = lane / L::LPE, ul = lane % L::LPE;
+  const int64_t unit = int64_t(blockIdx.x) * kEnvWaves + wave;
   // with one group per wave the center (hence e and every Y address) is
   // wave-uniform, so Y rows come through scalar loads
-  const int64_t n = L::G == 1 ? int64_t(blockIdx.x) : int64_t(blockIdx.x) * L::G + grp;
-  if (n >= N) return;
-  const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
+  const int64_t n0 = unit * L::G;  // the wave's first center
+  if (n0 >= N) return;
+  const int64_t n = n0 + (L::G == 1 ? 0 : grp);
+  const bool valid = n < N;
+  const int64_t e0 = valid ? row_ptr[n] : 0, e1 = valid ? row_ptr[n + 1] : 0;
   float acc[L::CPL][D2];
 #pragma unroll
   for (int t = 0; t < L::CPL; ++t)
@@ -162,8 +175,21 @@ __global__ __launch_bounds__(kWave) void env_embed_kernel(int64_t N, const int64
     for (int t = 0; t < L::CPL; ++t) wv[t] = w[e * U + ul + t * kWave];
     env_accumulate<U, D2, DET>(acc, wv, y);
   }
+  // The wave's env rows are one contiguous block (its centers are consecutive;
+  // lane l's row of channel group t sits at (l + 64 t) D2): staged in LDS and
+  // written as 16 bytes per lane along the block, rather than each lane's
+  // row on its own (every store instruction touching 64 partial lines).
+  float *rows = reinterpret_cast<float *>(rows4) + wave * RF;
 #pragma unroll
-  for (int t = 0; t < L::CPL; ++t) store_row<D2>(env + (n * U + ul + t * kWave) * D2, acc[t]);
+  for (int t = 0; t < L::CPL; ++t)
+#pragma unroll
+    for (int j = 0; j < D2; ++j) rows[(lane + kWave * t) * D2 + j] = acc[t][j];
+  lds_sync<1>();
+  const int64_t base = n0 * U * D2, total = N * U * D2;  // floats
+  float4 *dst = reinterpret_cast<float4 *>(env + base);
+#pragma unroll
+  for (int i = lane; i < RF / 4; i += kWave)
+    if (base + 4 * int64_t(i) < total) dst[i] = rows4[wave * (RF / 4) + i];
 }
 
 // -------------------------------------------------------------------- slabs
@@ -1694,7 +1720,7 @@ using BwdFn = void (*)(dim3, hipStream_t, const int64_t *, const float *, const 
 
 template <int U, int D2, bool DET>
 void launch_env(dim3 grid, hipStream_t s, int64_t N, const int64_t *rp, const float *w, const float *Y, float *env) {
-  hipLaunchKernelGGL((env_embed_kernel<U, D2, DET>), grid, dim3(kWave), 0, s, N, rp, w, Y, env);
+  hipLaunchKernelGGL((env_embed_kernel<U, D2, DET>), grid, dim3(kWave * kEnvWaves), 0, s, N, rp, w, Y, env);
 }
 
 template <class Core, int U>
@@ -1874,7 +1900,7 @@ int after_launch(const char *what) {
 
 // Blocks of 64 lanes: the env kernel packs 64/U centers per block when U < 64.
 unsigned env_blocks(int U, int64_t N) {
-  const int per = U < kWave ? kWave / U : 1;
+  const int64_t per = (U < kWave ? kWave / U : 1) * int64_t(kEnvWaves);  // centers per workgroup
   return unsigned((N + per - 1) / per);
 }
 
