@@ -730,7 +730,16 @@ __device__ __forceinline__ void embedding_vjp(const float *ge_l, float *stage, i
       for (int off = 1; off < 8; off *= 2)
 #pragma unroll
         for (int j = 0; j < D2; ++j) gy[j] += __shfl_xor(gy[j], off);
-      if (k < cnt && q == 0) store_row<D2>(grad_Y + (eb + k) * D2, gy);
+      // the batch's grad_Y rows are contiguous: staged in the (no longer
+      // needed) Y rows and stored by consecutive lanes, 256 bytes per
+      // instruction, instead of one lane per row
+      if (k < cnt && q == 0) {
+#pragma unroll
+        for (int j = 0; j < D2; ++j) yl[k * D2 + j] = gy[j];
+      }
+      lds_sync<1>();
+      float *gyb = grad_Y + eb * D2;
+      for (int i = lane; i < cnt * D2; i += kWave) gyb[i] = yl[i];
     }
   }
 }
