@@ -428,10 +428,11 @@ constexpr int kMFwdThreads = kWave * TPMFwd<Core::LMAX, Core::FULL>::NW;
 // that the rows' 16-byte accesses (lane r reads row r) put any 8 consecutive
 // lanes on 8 distinct 16-byte columns and any 16 on distinct bank groups of a
 // 256-byte span, without padding (the profiler counts no bank conflicts); the
-// result tile uses the same layout.  The waits for a tile's loads are explicit (the compiler does not
-// track loads into LDS): every iteration issues the same number of loads and
-// stores (past the segment their descriptors have no range), so the number
-// issued after tile k's loads is fixed.
+// result tile uses the same layout.  The waits for a tile's loads are
+// explicit (the compiler does not track loads into LDS): every iteration
+// issues the same number of loads and stores (past the segment their
+// descriptors have no range), so the number issued after tile k's loads is
+// fixed.
 template <class Core, int U, class MF>
 __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_ptr, const float *__restrict__ x,
                                                const float *__restrict__ env, const float *__restrict__ path_w,
@@ -448,6 +449,8 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
   constexpr int PER = TF4 / NT;              // loads (and stores) per thread and tile
   constexpr uint32_t EDGE_BYTES = U * D1 * 4;
   static_assert(D1 == 32 && U % kWave == 0 && TF4 % NT == 0 && D1 == NW * ROWS && ROWS == 4, "layout");
+  // position of 16-byte chunk q of tile row r
+  auto pos = [](int r, int q) { return r * R4 + (q ^ ((r & 7) ^ ((r >> 3) & 1))); };
   __shared__ float4 xb4[NB * TF4];
   __shared__ float4 os4[TF4];  // the result tile, laid out as the tile buffers
   const uint32_t xb_lds = uint32_t(reinterpret_cast<uintptr_t>((lds_void *)xb4));
@@ -479,7 +482,7 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
         const int blk = wave * PER + i, slot = blk * kWave + lane;
-        const int r = slot / R4, q = (slot % R4) ^ ((r & 7) ^ ((r >> 3) & 1));
+        const int r = slot / R4, q = pos(r, slot % R4) - r * R4;  // the chunk that lands at this slot
         const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(q) * 16;
         asm volatile("buffer_load_dwordx4 %0, %1, 0 offen nt lds"
                      :
@@ -523,11 +526,11 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
         float xr[D1], o[ROWS];
 #pragma unroll
         for (int q = 0; q < R4; ++q) {
-          const float4 a = xb[r * R4 + (q ^ ((r & 7) ^ ((r >> 3) & 1)))];
+          const float4 a = xb[pos(r, q)];
           xr[4 * q] = a.x; xr[4 * q + 1] = a.y; xr[4 * q + 2] = a.z; xr[4 * q + 3] = a.w;
         }
         MF::apply(wave, xr, m, o);
-        os4[r * R4 + (wave ^ ((r & 7) ^ ((r >> 3) & 1)))] = make_float4(o[0], o[1], o[2], o[3]);
+        os4[pos(r, wave)] = make_float4(o[0], o[1], o[2], o[3]);
       }
       lds_sync<NW>();
       const auto ro = tile_rsrc(out, k);
@@ -535,7 +538,7 @@ __device__ __forceinline__ void matrix_fwd_dma(const int64_t *__restrict__ row_p
       for (int i = 0; i < PER; ++i) {
         const int f = tid + NT * i, r = f / R4, c = f % R4;
         const uint32_t voff = uint32_t(r / kWave) * EDGE_BYTES + uint32_t(r % kWave) * (D1 * 4) + uint32_t(c) * 16;
-        const float4 v = os4[r * R4 + (c ^ ((r & 7) ^ ((r >> 3) & 1)))];
+        const float4 v = os4[pos(r, c)];
         __builtin_amdgcn_raw_buffer_store_b128(u32x4{__float_as_uint(v.x), __float_as_uint(v.y),
                                                      __float_as_uint(v.z), __float_as_uint(v.w)},
                                                ro, int(voff), 0, kNonTemporal);
