@@ -488,12 +488,15 @@ def test_handover_timeout_is_reported_and_ends(at, monkeypatch):
     assert block_rel_err(gpw.cpu().numpy(), t.path_weight_grad(data[0], data[1], renv, data[5])) <= BWD_TOL
 
 
-def test_train_backward_rejects_small_workspace(at):
-    plan = _plan(at, 1, 16, False)
+@pytest.mark.parametrize("lmax,U,full", [(1, 16, False), (3, 16, True), (3, 128, True)])
+def test_train_backward_rejects_small_workspace(at, lmax, U, full):
+    """Per-center rows (lmax < 3) or the matrix-core kernel's per-wave rows (lmax 3):
+    a workspace one float4 short of the size the query gives is rejected before any launch."""
+    plan = _plan(at, lmax, U, full)
     rp = torch.tensor([0, 2], dtype=torch.int64, device=DEV)
-    x = torch.zeros((2, 16, plan.d1), device=DEV)
-    w, y = torch.zeros((2, 16), device=DEV), torch.zeros((2, plan.d2), device=DEV)
-    env, pw = torch.zeros((1, 16, plan.d2), device=DEV), torch.zeros((plan.n_paths, 16), device=DEV)
+    x = torch.zeros((2, U, plan.d1), device=DEV)
+    w, y = torch.zeros((2, U), device=DEV), torch.zeros((2, plan.d2), device=DEV)
+    env, pw = torch.zeros((1, U, plan.d2), device=DEV), torch.zeros((plan.n_paths, U), device=DEV)
     ws = torch.empty(at.allegro_tp_backward_workspace(plan, 1) - 16, dtype=torch.uint8, device=DEV)
     with pytest.raises(at.AllegroError) as ex:
         at.allegro_tp_backward_train(plan, rp, x, env, pw, x, w, y, workspace=ws)
