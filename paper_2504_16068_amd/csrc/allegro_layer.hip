@@ -558,6 +558,13 @@ __global__ __launch_bounds__(kMixThreads) void mix_kernel(int64_t E, const float
 }
 
 constexpr int kWgEdges = 4;        // edges per tile: column counts NE * (2l + 1) are multiples of 4
+// Channel u of the column of component k sits at u ^ wg_swizzle(k) (bits 1-3,
+// within its 16-channel block).  A memory wave's 4-byte writes of one
+// instruction cover 8 components k = 4 b + q (b = 0..7) of up to 8 channels;
+// the swizzle spreads them over 64 distinct banks (without it 8 lanes shared
+// a bank), and the compute waves' reads of 16 consecutive channels of one
+// column stay a permutation of one 16-bank block.
+__host__ __device__ constexpr int wg_swizzle(int k) { return 2 * (k >> 2); }
 constexpr int kWgCS = kU + 16;     // = 16 (mod 64): the four lane groups of an operand read hit distinct banks
 constexpr int kWgThreads = 512;    // four compute waves, then four memory waves
 
@@ -599,9 +606,12 @@ __device__ __forceinline__ void wgrad_compute_role(int64_t n_tiles, float *lds, 
       const int q0 = base + (l / 16) * (nq / 4);
 #pragma unroll
       for (int s = 0; s < nq / 4; ++s) {
-        const float a = la[(q0 + s) * CS + 16 * w + l % 16];
+        // column q0 + s holds component off(c) + s (of edge l / 16): its
+        // channels sit XOR-swizzled by wg_swizzle of that component
+        const int ul = (l % 16) ^ wg_swizzle(X::off(c) + s);
+        const float a = la[(q0 + s) * CS + 16 * w + ul];
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[c][nt] = mfma_16x16x4(a, lb[(q0 + s) * CS + 16 * nt + l % 16], acc[c][nt]);
+        for (int nt = 0; nt < 4; ++nt) acc[c][nt] = mfma_16x16x4(a, lb[(q0 + s) * CS + 16 * nt + ul], acc[c][nt]);
       }
     });
     lds_sync<8>();  // this buffer is free again; the other holds the next tile
@@ -637,7 +647,7 @@ __device__ __forceinline__ void wgrad_memory_role(int64_t E, int64_t n_tiles, co
         const int e = idx / (U * D1), rem = idx % (U * D1), u = rem / D1, k = rem % D1;
         int col0, dim;
         component_column<X>(k, NE, col0, dim);
-        a = (col0 + e * dim) * M::CS + u;
+        a = (col0 + e * dim) * M::CS + (u ^ wg_swizzle(k));
       }
       addr[i][q] = a;
     }
