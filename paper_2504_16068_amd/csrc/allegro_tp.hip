@@ -203,6 +203,14 @@ __global__ __launch_bounds__(kWave * kEnvWaves) void env_embed_kernel(int64_t N,
 template <int D>
 struct TileShape {
   static constexpr int SF4 = 16 * D;  // float4 per slab (64 rows of D floats)
+  // In LDS, 32-float rows are padded to 36 floats, so that the 16-byte reads
+  // of eight consecutive lanes' rows (lane r reads row r) hit distinct banks;
+  // unpadded, 128-byte rows put all eight on one bank group.  Other widths
+  // are odd multiples of a word or short enough to stay as they are.
+  static constexpr int RS = D == 32 ? 36 : D;  // LDS row stride (floats)
+  static constexpr int LF4 = 16 * RS;          // LDS float4 per slab
+  // LDS position of float4 f of a slab
+  static __device__ __forceinline__ int pos(int f) { return D == 32 ? f + (f >> 3) : f; }
 };
 
 template <int U>
@@ -250,9 +258,9 @@ __device__ __forceinline__ void tile_load(const float *__restrict__ src, float4 
       if (lane + kWave * KF < TF4) v[KF] = load_stream(base + lane + kWave * KF);
     }
 #pragma unroll
-    for (int k = 0; k < KF; ++k) tile[lane + kWave * k] = v[k];
+    for (int k = 0; k < KF; ++k) tile[TileShape<D>::pos(lane + kWave * k)] = v[k];
     if constexpr (PER > KF) {
-      if (lane + kWave * KF < TF4) tile[lane + kWave * KF] = v[KF];
+      if (lane + kWave * KF < TF4) tile[TileShape<D>::pos(lane + kWave * KF)] = v[KF];
     }
   } else {
 #pragma unroll
@@ -263,7 +271,7 @@ __device__ __forceinline__ void tile_load(const float *__restrict__ src, float4 
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int f = lane + kWave * k;
-      if (f < n_f4) tile[f] = v[k];
+      if (f < n_f4) tile[TileShape<D>::pos(f)] = v[k];
     }
   }
 }
@@ -276,15 +284,15 @@ __device__ __forceinline__ void tile_store(float *__restrict__ dst, const float4
   float4 *base = reinterpret_cast<float4 *>(dst) + tile_base<U, D>(e0, e1, s0, cnt, t, n_f4);
   if (n_f4 == TF4) {
 #pragma unroll
-    for (int k = 0; k < KF; ++k) store_stream(tile[lane + kWave * k], base + lane + kWave * k);
+    for (int k = 0; k < KF; ++k) store_stream(tile[TileShape<D>::pos(lane + kWave * k)], base + lane + kWave * k);
     if constexpr (PER > KF) {
-      if (lane + kWave * KF < TF4) store_stream(tile[lane + kWave * KF], base + lane + kWave * KF);
+      if (lane + kWave * KF < TF4) store_stream(tile[TileShape<D>::pos(lane + kWave * KF)], base + lane + kWave * KF);
     }
   } else {
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int f = lane + kWave * k;
-      if (f < n_f4) store_stream(tile[f], base + f);
+      if (f < n_f4) store_stream(tile[TileShape<D>::pos(f)], base + f);
     }
   }
 }
@@ -362,10 +370,10 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
   constexpr int D1 = Core::D1, D2 = Core::D2, WPT = NW / L::CPL;
   constexpr int TF4 = TileShape<D1>::SF4;  // one slab per tile
   static_assert(NW % L::CPL == 0, "waves split evenly over the channel halves");
-  __shared__ float4 tiles[NW * TF4];
+  __shared__ float4 tiles[NW * TileShape<D1>::LF4];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, ul = lane % L::LPE;
   const int t = wave / WPT, first = wave % WPT;
-  float4 *tile = tiles + wave * TF4;
+  float4 *tile = tiles + wave * TileShape<D1>::LF4;
   float *tile_f = reinterpret_cast<float *>(tile);
   const int64_t n = blockIdx.x;
   const int64_t e0 = row_ptr[n], e1 = row_ptr[n + 1];
@@ -379,7 +387,7 @@ __global__ __launch_bounds__(kWave * NW) __attribute__((amdgpu_waves_per_eu(Kern
     tile_load<U, D1, TF4>(x, tile, e0, e1, s, 1, t, lane);
     lds_sync<1>();
     if (row_valid<U>(e0, e1, s, lane)) {
-      float *row = tile_f + lane * D1;
+      float *row = tile_f + lane * TileShape<D1>::RS;
       float xr[D1], orow[D1];
 #pragma unroll
       for (int i = 0; i < D1; ++i) xr[i] = row[i];
@@ -799,8 +807,8 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
     lds_sync<1>();
     if (row_valid<U>(e0, e1, s, lane)) {
       // x row in, grad_x row out, in place in the LDS tile
-      float *row = tx + lane * D1;
-      const float *grow = tg + lane * D1;
+      float *row = tx + lane * TileShape<D1>::RS;
+      const float *grow = tg + lane * TileShape<D1>::RS;
       if constexpr (WG) Core::wgrad(row, er, grow, sw);
       Core::bwd(row, er, wr, grow, row, ge);
     }
@@ -818,7 +826,7 @@ __device__ __forceinline__ void bwd_pass1(const float *__restrict__ x, const flo
 template <class Core, int U, bool WG, int NW_>
 struct BwdLds {
   static constexpr int NW = NW_, D2 = Core::D2, NP = Core::NP;
-  static constexpr int TILE_F4 = TileShape<Core::D1>::SF4;
+  static constexpr int TILE_F4 = TileShape<Core::D1>::LF4;  // LDS float4 of one tile
   static constexpr int EB = 8;          // edges per pass-2 batch of one wave (8 lanes per edge)
   static constexpr int WROW = U + 1;    // padded w row: per-lane row reads hit distinct banks
   static constexpr int P1 = NW * 2 * TILE_F4 * 4;
