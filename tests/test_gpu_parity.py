@@ -174,6 +174,21 @@ def test_edge_cases(at, lmax, full, U, degrees):
     assert np.all(env[np.asarray(degrees) == 0] == 0)
 
 
+@pytest.mark.parametrize("U", [64, 128])
+def test_matrix_forward_tile_boundaries(at, U):
+    """The lmax-3 full-parity forward loads 4-edge tiles straight into LDS through
+    a ring of four buffers: segment lengths on every side of a tile boundary (0 to
+    5, 7 to 9, 12 and 13, 16 and 17, 20 and 21), a ring that wraps several times
+    (33, 64, 65 edges), and the backward on the same data, against the oracle."""
+    degrees = [0, 1, 2, 3, 4, 5, 7, 8, 9, 12, 13, 16, 17, 20, 21, 33, 64, 65, 0]
+    _note(f"[gpu] matrix forward tile boundaries U={U}")
+    data = _synthetic(3, True, U, degrees, seed=4242 + U)
+    plan = _plan(at, 3, U, True)
+    gpu = _np(_run_gpu(at, plan, *data))
+    t, *ref = _oracle(3, True, *data)
+    _compare(t, gpu, ref, f"lmax3F U{U} tile boundaries")
+
+
 ALL_SHAPES = [(lmax, full, U) for lmax in (1, 2, 3) for full in (False, True) for U in (16, 32, 64, 128)]
 
 
